@@ -1,0 +1,169 @@
+"""Pins of the oracle's capacity rule (Eq. 4, dynamic capacity factors) and
+slot assignment / drop rule (Section 3.1) against exact rationals, the
+quadratic brute-force definition and invariants."""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+
+# -- capacity -----------------------------------------------------------------
+@pytest.mark.parametrize("name,expect", [("c1", 80), ("c2", 1024), ("c3", 512)])
+def test_static_capacity_worked_values(name, expect):
+    """ceil(alpha * T * k / E) for the static runs of the named workloads."""
+    wl = W.config(name)
+    kind, num, den = wl.capacity[0]
+    assert kind == "static"
+    cap = O.capacity_static(wl.T, wl.k, wl.E, num, den)
+    assert (cap == expect).all()
+    assert expect == math.ceil(Fraction(num, den) * wl.T * wl.k / wl.E)
+
+
+def test_static_capacity_half_and_clamps():
+    assert O.capacity_static(256, 1, 4, 1, 2)[0] == 32
+    assert O.capacity_static(10, 2, 1, 7, 1)[0] == 10          # clamp to T
+    assert O.capacity_static(10, 1, 8, 1, 100, cap_min=3)[0] == 3
+
+
+def test_dynamic_capacity_exact_rational():
+    counts = np.arange(0, 200001)
+    for num, den in [(11, 10), (21, 20), (1, 1), (5, 4)]:
+        got = O.capacity_dynamic(counts, T=10 ** 9, num=num, den=den)
+        ref = np.array([math.ceil(Fraction(num * int(c), den)) for c in counts[::997]])
+        np.testing.assert_array_equal(got[::997], ref)
+        # spot the cases a float64 ceil gets wrong (e.g. 1.1 * 50 -> 56)
+        for c in (50, 90, 100, 1000):
+            assert got[c] == math.ceil(Fraction(num * c, den))
+    assert math.ceil(1.1 * 50) == 56 and O.capacity_dynamic([50], 10 ** 6, 11, 10)[0] == 55
+    np.testing.assert_array_equal(O.capacity_dynamic([0, 5, 9], T=6, num=11, den=10, cap_min=2),
+                                  [2, 6, 6])
+
+
+def test_offsets():
+    np.testing.assert_array_equal(O.exclusive_offsets([3, 0, 5]), [0, 3, 3, 8])
+
+
+# -- slots ---------------------------------------------------------------------
+def _brute_slots(ids, E, cap, off, rows_alloc):
+    """pos(t,j) = number of live assignments to the same expert that come
+    earlier in priority order (all j=0 in token order, then j=1, ...)."""
+    T, k = ids.shape
+    live, status = O.validate_assignments(ids, E)
+    order = [(t, j) for j in range(k) for t in range(T)]
+    dest = -np.ones((T, k), dtype=np.int64)
+    for n, (t, j) in enumerate(order):
+        if not live[t, j]:
+            continue
+        e = ids[t, j]
+        pos = sum(1 for (t2, j2) in order[:n] if live[t2, j2] and ids[t2, j2] == e)
+        room = max(0, min(cap[e], off[e + 1] - off[e], rows_alloc - off[e])) if off[e] >= 0 else 0
+        if pos < room:
+            dest[t, j] = off[e] + pos
+    return dest
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_slots_match_quadratic_definition(seed):
+    rng = np.random.default_rng(100 + seed)
+    T = int(rng.integers(1, 9))
+    E = int(rng.integers(1, 6))
+    k = int(rng.integers(1, min(E, 3) + 1))
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    if seed % 3 == 0:                                      # cached-id faults
+        ids[0, 0] = E + 2
+        if k > 1:
+            ids[-1, 1] = ids[-1, 0]
+    cap = rng.integers(0, T + 1, size=E)
+    off = O.exclusive_offsets(cap)
+    rows_alloc = int(off[-1])
+    if seed % 4 == 1:
+        rows_alloc = max(0, rows_alloc - 2)                # region overflow
+    s = O.assign_slots(ids, E, cap, off, rows_alloc)
+    np.testing.assert_array_equal(s["dest_row"], _brute_slots(ids, E, cap, off, rows_alloc))
+
+
+def _check_invariants(ids, E, cap, off, rows_alloc, s):
+    T, k = ids.shape
+    live, _ = O.validate_assignments(ids, E)
+    dest, counts, fill = s["dest_row"], s["counts"], s["fill"]
+    assert counts.sum() == live.sum()
+    assert fill.sum() == (dest >= 0).sum()
+    assert (fill <= np.maximum(cap, 0)).all()
+    kept = dest[dest >= 0]
+    assert len(np.unique(kept)) == len(kept)
+    for e in range(E):
+        rows = sorted(dest[(ids == e) & (dest >= 0)] - off[e])
+        assert rows == list(range(fill[e]))                # first entries are used
+    src = s["src"]
+    for t in range(T):
+        for j in range(k):
+            if dest[t, j] >= 0:
+                assert src[dest[t, j]] == t * k + j
+    assert (src >= 0).sum() == len(kept)
+
+
+def test_slot_invariants_and_monotonicity():
+    rng = np.random.default_rng(7)
+    T, E, k = 400, 6, 2
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    counts = O.count_assignments(ids, E)
+    assert counts.sum() == T * k
+    for cap in [np.zeros(E, np.int64), rng.integers(0, 200, E), counts, counts + 3,
+                np.full(E, T)]:
+        off = O.exclusive_offsets(cap)
+        s = O.assign_slots(ids, E, cap, off, int(off[-1]))
+        _check_invariants(ids, E, cap, off, int(off[-1]), s)
+        np.testing.assert_array_equal(s["counts"], counts)
+        if (cap >= counts).all():
+            assert (s["dest_row"] >= 0).all()             # enough room: no drops
+        # raising any capacity never un-keeps an assignment
+        cap2 = cap + rng.integers(0, 5, E)
+        off2 = O.exclusive_offsets(cap2)
+        s2 = O.assign_slots(ids, E, cap2, off2, int(off2[-1]))
+        assert ((s["dest_row"] >= 0) <= (s2["dest_row"] >= 0)).all()
+
+
+def test_priority_first_choices_before_second():
+    # expert 0 has capacity 2: token 2's first choice beats token 0's second
+    ids = np.array([[1, 0], [0, 1], [0, 2]], dtype=np.int32)
+    cap = np.array([2, 5, 5])
+    s = O.assign_slots(ids, 3, cap, O.exclusive_offsets(cap), 12)
+    np.testing.assert_array_equal(s["dest_row"], [[2, -1], [0, 3], [1, 7]])
+    np.testing.assert_array_equal(s["fill"], [2, 2, 1])
+    np.testing.assert_array_equal(s["counts"], [3, 2, 1])
+
+
+def test_status_bits_and_all_to_one_expert():
+    ids = np.array([[0, 0], [5, 1], [-1, 1]], dtype=np.int32)
+    cap = np.array([4, 4])
+    s = O.assign_slots(ids, 2, cap, O.exclusive_offsets(cap), 8)
+    assert s["status"] == O.STATUS_BAD_ID | O.STATUS_DUP_ID
+    np.testing.assert_array_equal(s["dest_row"], [[0, -1], [-1, 4], [-1, 5]])
+    np.testing.assert_array_equal(s["counts"], [1, 2])
+    s = O.assign_slots(np.array([[0], [0]], np.int32), 1, np.array([3]), np.array([0, 3]), 1)
+    assert s["status"] == O.STATUS_REGION and list(s["dest_row"][:, 0]) == [0, -1]
+    ids = np.zeros((50, 1), np.int32)                       # all tokens to one expert
+    cap = np.array([20, 20, 20])
+    s = O.assign_slots(ids, 3, cap, O.exclusive_offsets(cap), 60)
+    assert list(s["fill"]) == [20, 0, 0] and (s["dest_row"][:20, 0] == np.arange(20)).all()
+    assert (s["dest_row"][20:] == -1).all()
+
+
+def test_dispatch_is_exact_copy():
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal((30, 5))
+    ids = np.stack([rng.permutation(4)[:2] for _ in range(30)]).astype(np.int32)
+    cap = np.array([9, 20, 3, 40])
+    off = O.exclusive_offsets(cap)
+    s = O.assign_slots(ids, 4, cap, off, int(off[-1]))
+    xd = O.dispatch_rows(x, s["dest_row"], int(off[-1]))
+    for t in range(30):
+        for j in range(2):
+            r = s["dest_row"][t, j]
+            if r >= 0:
+                assert (xd[r] == x[t]).all()
+    assert np.isnan(xd[s["src"] < 0]).all()
