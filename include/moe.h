@@ -1,0 +1,268 @@
+/*
+ * moe.h - C ABI of libmoe, an MI355X (gfx950) implementation of one
+ * capacity-bounded top-k Mixture-of-Experts layer with dynamic per-expert
+ * capacities and a cached-assignment (gate bypass) path, forward and
+ * backward.  Method: Kossmann, Jia, Aiken, "Optimizing Mixture of Experts
+ * using Dynamic Recompilations" (MLSys 2022): Algorithm 1 (top-k MoE
+ * forward), Eq. 1 (weighted sum of expert outputs), Eq. 4 and Section 3.1
+ * (expert capacity, drops, dynamic capacity factors), Section 3.2 (sample
+ * assignment caching).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - `stream` is a hipStream_t (NULL = the legacy default stream).  Every
+ *   call only enqueues work on it and never synchronises; results are
+ *   ready when the stream reaches that point.
+ * - Pointers are DEVICE pointers unless a parameter is marked [host].  The
+ *   caller owns all memory, including scratch `workspace` buffers sized by
+ *   the matching *_workspace_bytes query.  The library keeps no state.
+ * - Argument errors (bad sizes, NULL pointers, unsupported combinations,
+ *   a workspace that is too small) are reported synchronously through the
+ *   returned moe_status and nothing is enqueued.  Errors that depend on
+ *   device data (bad cached ids, capacity regions that do not fit) never
+ *   abort: the offending assignment is dropped and a bit is OR-ed into the
+ *   caller's device `status` word (the caller zeroes it beforehand).
+ * - Layer tensors (x, weights, activations, outputs) are row-major in the
+ *   layer dtype `dt`: MOE_F32 (float) or MOE_BF16 (bf16 bit patterns,
+ *   uint16).  Gate logits, probabilities, combine weights and every weight
+ *   gradient are float32.  Accumulation is float32 in both dtypes.
+ * - Weights are stored output-features x input-features, the layout of a
+ *   linear map y = x W^T: w_g [E,d], w1 [E,f,d], w3 [E,f,d], w2 [E,d,f].
+ * - Limits: 1 <= E <= 64, 1 <= k <= min(E, 8), T >= 0 (T = 0 is a valid
+ *   empty batch), d, f >= 1 and multiples of 8, T*k and rows_alloc < 2^31.
+ * - Every output is deterministic run to run (no floating-point atomics).
+ */
+#ifndef MOE_H_
+#define MOE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOE_OK = 0,
+  MOE_EINVAL = 1,        /* bad size, NULL pointer or flag */
+  MOE_EUNSUPPORTED = 2,  /* valid request this build does not implement */
+  MOE_EHIP = 3,          /* a HIP launch failed */
+  MOE_EWORKSPACE = 4     /* workspace NULL or smaller than the query said */
+} moe_status;
+
+typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
+
+typedef enum { MOE_RELU = 0, MOE_GELU_TANH = 1, MOE_SWIGLU = 2 } moe_act;
+
+/* Bits OR-ed into the device status word. */
+#define MOE_STATUS_BAD_ID 1 /* a cached expert id outside [0, E) */
+#define MOE_STATUS_DUP_ID 2 /* a token names the same expert twice */
+#define MOE_STATUS_REGION 4 /* an expert's capacity region does not fit */
+
+/* Human-readable name of a moe_status value. [host] */
+const char* moe_status_string(int status);
+
+/* ABI version (incremented on incompatible change). [host] */
+int moe_abi_version(void);
+
+/*
+ * moe_gate_topk - Algorithm 1, first three steps: score <- G(x),
+ * indices <- argmax_k(score), (w_1..w_k) <- normalize(score[indices]),
+ * for a linear gate G(x) = x w_g^T + bias.
+ *   x       [T,d]  layer dtype
+ *   w_g     [E,d]  layer dtype
+ *   bias    [E]    float32, or NULL for no bias
+ *   logits  [T,E]  float32 out: the gate scores
+ *   ids     [T,k]  int32 out: the k largest logits per token, largest first;
+ *                  equal logits go to the lower expert index
+ *   weights [T,k]  float32 out: p = softmax(logits); renorm != 0 gives
+ *                  p[ids]/sum p[ids] (the normalisation of Algorithm 1,
+ *                  used for k >= 2); renorm == 0 gives the raw p[ids]
+ *                  (Switch-style k = 1).
+ */
+moe_status moe_gate_topk(void* stream, moe_dtype dt, int T, int d, int E, int k,
+                         int renorm, const void* x, const void* w_g,
+                         const float* bias, float* logits, int32_t* ids,
+                         float* weights);
+
+/*
+ * moe_count - the per-expert load that dynamic capacity factors follow
+ * (Section 3.1: how many samples the gate assigns to each expert), before
+ * any capacity is applied.
+ *   ids    [T,k] int32 expert ids (gate output or cached)
+ *   counts [E]   int32 out: live assignments per expert.  An id outside
+ *                [0,E) is not counted (status bit 1); a repeat of an
+ *                expert already named by the token at a lower j is not
+ *                counted (status bit 2).
+ *   status [1]   int32 in/out, bits OR-ed in.
+ */
+moe_status moe_count(void* stream, int T, int E, int k, const int32_t* ids,
+                     int32_t* counts, int32_t* status);
+
+/*
+ * moe_update_capacity - Eq. 4 and Section 3.1: per-expert capacities and
+ * the row layout of the grouped expert buffer.
+ *   counts == NULL: static capacity factor alpha = num/den,
+ *                   C_e = ceil(num*T*k / (den*E)) for every expert;
+ *   counts != NULL: dynamic capacity factors, C_e = ceil(num*counts[e]/den)
+ *                   (num/den is the margin over the observed load; 1/1 is
+ *                   exact capacity).
+ * Computed in exact 64-bit integer arithmetic, then clamped to [cap_min, T].
+ *   capacity [E]   int32 out
+ *   offsets  [E+1] int32 out: offsets[e] = sum of C of experts < e, so
+ *                  expert e owns rows [offsets[e], offsets[e]+C_e);
+ *                  offsets[E] is the rows the layout needs (the caller's
+ *                  rows_alloc must be at least that).
+ * num, den >= 1; cap_min >= 0.
+ */
+moe_status moe_update_capacity(void* stream, int T, int k, int E,
+                               const int32_t* counts, int num, int den,
+                               int cap_min, int32_t* capacity,
+                               int32_t* offsets);
+
+/* Workspace bytes of moe_dispatch for these sizes. [host] */
+size_t moe_dispatch_workspace_bytes(int T, int E, int k);
+
+/*
+ * moe_dispatch - GroupBy with the capacity/drop rule of Section 3.1: each
+ * expert's tensor is filled from its first entry, assignments beyond the
+ * expert's capacity are dropped.  Priority: all first choices in token
+ * order, then all second choices, and so on.
+ *   x         [T,d]          layer dtype
+ *   ids       [T,k]          int32 expert ids (gate output or cached ids:
+ *                            the gate-bypass path of Section 3.2)
+ *   capacity  [E], offsets [E+1]  as written by moe_update_capacity
+ *   rows_alloc                rows of the grouped buffers
+ *   counts    [E]   out: live assignments per expert (as moe_count)
+ *   fill      [E]   out: kept assignments per expert, min(counts, C_e)
+ *   dest_row  [T,k] out: row of x_disp holding (t,j), or -1 if dropped
+ *   src       [rows_alloc] out: t*k+j of the assignment in that row, or -1
+ *   x_disp    [rows_alloc,d] out: x_disp[dest_row[t,j]] = x[t] (exact
+ *             copy); rows without an assignment are left untouched.
+ *   status    [1] in/out: bits 1, 2 as moe_count; bit 4 when an expert's
+ *             region [offsets[e], offsets[e]+C_e) overlaps the next one or
+ *             runs past rows_alloc (the region is cut to what fits).
+ *   workspace moe_dispatch_workspace_bytes(T,E,k) bytes.
+ */
+moe_status moe_dispatch(void* stream, moe_dtype dt, int T, int d, int E, int k,
+                        const void* x, const int32_t* ids,
+                        const int32_t* capacity, const int32_t* offsets,
+                        int64_t rows_alloc, int32_t* counts, int32_t* fill,
+                        int32_t* dest_row, int32_t* src, void* x_disp,
+                        int32_t* status, void* workspace,
+                        size_t workspace_bytes);
+
+/* Workspace bytes of moe_expert_ffn_fwd / moe_expert_ffn_bwd. [host] */
+size_t moe_ffn_fwd_workspace_bytes(moe_dtype dt, moe_act act, int E, int d,
+                                   int f, int64_t rows_alloc);
+size_t moe_ffn_bwd_workspace_bytes(moe_dtype dt, moe_act act, int E, int d,
+                                   int f, int64_t rows_alloc);
+
+/*
+ * moe_expert_ffn_fwd - the expert modules E_e(x) of Algorithm 1, run on each
+ * expert's own rows only (dynamically sized expert tensors, Section 3.1).
+ * For expert e the rows are [offsets[e], offsets[e]+rows[e]) of the grouped
+ * buffers; rows[e] is clamped to the expert's region and to rows_alloc.
+ *   MOE_RELU / MOE_GELU_TANH: H = X w1_e^T, A = act(H), Y = A w2_e^T
+ *   MOE_SWIGLU:  H1 = X w1_e^T, H3 = X w3_e^T, A = silu(H1)*H3, Y = A w2_e^T
+ * bf16 layers round H (H1, H3), A and Y to bf16; A is computed from the
+ * rounded H.  No bias.
+ *   offsets [E+1], rows [E] int32 (rows = fill: the method; rows = capacity:
+ *           a padded static-shape baseline)
+ *   x_disp  [rows_alloc,d], w1/w3 [E,f,d] (w3 NULL unless SwiGLU), w2 [E,d,f]
+ *   h_save  NULL for inference, else out: H [rows_alloc,f], or for SwiGLU
+ *           H1 then H3, [2,rows_alloc,f]; moe_expert_ffn_bwd reads it.
+ *   y_disp  [rows_alloc,d] out.  Rows outside every expert's rows are left
+ *           untouched.
+ */
+moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act, int E,
+                              int d, int f, const int32_t* offsets,
+                              const int32_t* rows, int64_t rows_alloc,
+                              const void* x_disp, const void* w1,
+                              const void* w3, const void* w2, void* h_save,
+                              void* y_disp, void* workspace,
+                              size_t workspace_bytes);
+
+/*
+ * moe_combine - Aggregate (Algorithm 1's weighted sum, Eq. 1):
+ * y[t] = sum over kept j, in order j = 0..k-1, of weights[t,j] *
+ * y_disp[dest_row[t,j]], summed in float32 and rounded once.  A token with
+ * no kept assignment gets 0 (dropped samples contribute nothing).
+ *   y_disp [rows_alloc,d], dest_row [T,k], weights [T,k] f32, y [T,d] out.
+ */
+moe_status moe_combine(void* stream, moe_dtype dt, int T, int d, int k,
+                       int64_t rows_alloc, const void* y_disp,
+                       const int32_t* dest_row, const float* weights, void* y);
+
+/*
+ * moe_combine_bwd - backward of moe_combine.  Dropped assignments get zero
+ * gradient (Section 3.1).
+ *   dy       [T,d] upstream gradient
+ *   dweights [T,k] f32 out: <dy[t], y_disp[dest_row[t,j]]> if kept, else 0
+ *   dy_disp  [rows_alloc,d] out: dy_disp[dest_row[t,j]] = weights[t,j]*dy[t]
+ *            (rounded to the layer dtype); other rows untouched.
+ */
+moe_status moe_combine_bwd(void* stream, moe_dtype dt, int T, int d, int k,
+                           int64_t rows_alloc, const void* dy,
+                           const void* y_disp, const int32_t* dest_row,
+                           const float* weights, void* dy_disp,
+                           float* dweights);
+
+/*
+ * moe_expert_ffn_bwd - backward of moe_expert_ffn_fwd over the same rows.
+ *   dA = dY w2_e;  RELU/GELU: dH = dA * act'(H) (relu'(0) = 0);
+ *   SWIGLU: dH1 = dA * H3 * silu'(H1), dH3 = dA * silu(H1)
+ *   (bf16 layers round dH, dH1, dH3);
+ *   dw2_e = dY^T A,  dw1_e = dH1^T X,  dw3_e = dH3^T X  (float32; an expert
+ *   with no rows gets zeros);  dx_disp = dH1 w1_e + dH3 w3_e (one rounding).
+ *   h_save   as written by moe_expert_ffn_fwd
+ *   dy_disp  [rows_alloc,d] (moe_combine_bwd output)
+ *   dx_disp  [rows_alloc,d] out (rows outside every expert's rows untouched)
+ *   dw1 [E,f,d], dw3 [E,f,d] (NULL unless SwiGLU), dw2 [E,d,f] float32 out,
+ *   fully overwritten.
+ */
+moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act, int E,
+                              int d, int f, const int32_t* offsets,
+                              const int32_t* rows, int64_t rows_alloc,
+                              const void* x_disp, const void* h_save,
+                              const void* w1, const void* w3, const void* w2,
+                              const void* dy_disp, void* dx_disp, float* dw1,
+                              float* dw3, float* dw2, void* workspace,
+                              size_t workspace_bytes);
+
+/* Workspace bytes of moe_gate_bwd. [host] */
+size_t moe_gate_bwd_workspace_bytes(int T, int d, int E);
+
+/*
+ * moe_gate_bwd - backward of moe_gate_topk through normalize() and the
+ * softmax (top-k indices are piecewise constant: no gradient).
+ *   raw (renorm = 0): g_j = dweights[t,j]
+ *   renorm:           g_j = (dweights_j - sum_i dweights_i w_i) / S,
+ *                     S = sum_j p[ids_j], w_j = p[ids_j]/S
+ *   dp[t,e] = sum_j [ids[t,j] = e] g_j;  dlogits = p * (dp - <dp, p>)
+ *   dw_g[e,i] = sum_t dlogits[t,e] x[t,i]  (float32, fixed summation order)
+ *   logits [T,E] (moe_gate_topk output), ids [T,k], dweights [T,k]
+ *   dlogits [T,E] f32 out, dw_g [E,d] f32 out (fully overwritten).
+ */
+moe_status moe_gate_bwd(void* stream, moe_dtype dt, int T, int d, int E, int k,
+                        int renorm, const void* x, const float* logits,
+                        const int32_t* ids, const float* dweights,
+                        float* dlogits, float* dw_g, void* workspace,
+                        size_t workspace_bytes);
+
+/*
+ * moe_dispatch_bwd - backward of moe_dispatch plus the gate's input term:
+ * dx[t] = sum over kept j of dx_disp[dest_row[t,j]]  (+ dlogits[t] . w_g
+ * when dlogits and w_g are both non-NULL; both NULL on the cached path),
+ * summed in float32, rounded once.  dx [T,d] out, fully overwritten.
+ */
+moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d, int E,
+                            int k, int64_t rows_alloc, const void* dx_disp,
+                            const int32_t* dest_row, const float* dlogits,
+                            const void* w_g, void* dx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H_ */

@@ -1,0 +1,532 @@
+// Load counting, capacities, slot assignment + dispatch (GroupBy with the
+// Section 3.1 capacity/drop rule), combine (Aggregate) and their backward.
+//
+// Slot assignment is a stable counting sort of the T*k assignments in
+// priority order q = j*T + t (all first choices in token order, then all
+// second choices, ...):
+//   1. per-chunk expert histograms (4096 assignments per workgroup),
+//   2. one workgroup scans them into per-chunk bases and applies capacity,
+//   3. each chunk re-ranks its assignments with wavefront ballots (expert id
+//      equality masks from 6 ballots, rank = popcount below the lane),
+//      giving pos, keep, dest_row and src - all integer, bit-exact.
+// The row copies (dispatch gather, combine, their backward) are token-major:
+// one wavefront per token, 16-byte vector loads/stores along the row, so x
+// is read once even when k rows are written.
+
+#include "common.hpp"
+#include "validate.hpp"
+
+namespace moe {
+namespace {
+
+constexpr int kChunk = 4096;  // assignments per workgroup in the routing kernels
+
+// Is assignment (t, j) live?  Sets status bits when `status` is non-null.
+__device__ __forceinline__ bool live_assignment(const int32_t* __restrict__ ids, int t,
+                                                int j, int k, int E, int32_t* status) {
+  const int32_t* row = ids + static_cast<size_t>(t) * k;
+  const int e = row[j];
+  if (e < 0 || e >= E) {
+    if (status) atomicOr(status, MOE_STATUS_BAD_ID);
+    return false;
+  }
+  for (int jj = 0; jj < j; ++jj) {
+    if (row[jj] == e) {
+      if (status) atomicOr(status, MOE_STATUS_DUP_ID);
+      return false;
+    }
+  }
+  return true;
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+  int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// counts[e] += live assignments of this block's chunk (counts zeroed before)
+__global__ __launch_bounds__(256) void count_kernel(const int32_t* __restrict__ ids, int T,
+                                                    int E, int k, int32_t* counts,
+                                                    int32_t* status) {
+  __shared__ int h[kMaxE];
+  if (threadIdx.x < kMaxE) h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t n = static_cast<int64_t>(T) * k;
+  const int64_t q0 = static_cast<int64_t>(blockIdx.x) * kChunk;
+  const int64_t q1 = min(n, q0 + kChunk);
+  for (int64_t q = q0 + threadIdx.x; q < q1; q += 256) {
+    const int j = static_cast<int>(q / T), t = static_cast<int>(q - static_cast<int64_t>(j) * T);
+    if (live_assignment(ids, t, j, k, E, status)) atomicAdd(&h[ids[static_cast<size_t>(t) * k + j]], 1);
+  }
+  __syncthreads();
+  if (threadIdx.x < E && h[threadIdx.x]) atomicAdd(&counts[threadIdx.x], h[threadIdx.x]);
+}
+
+// Eq. 4 / dynamic capacity factors, exact 64-bit integer ceil, + offsets.
+__global__ __launch_bounds__(64) void capacity_kernel(int T, int k, int E,
+                                                      const int32_t* __restrict__ counts,
+                                                      int num, int den, int cap_min,
+                                                      int32_t* __restrict__ capacity,
+                                                      int32_t* __restrict__ offsets) {
+  __shared__ int64_t c[kMaxE];
+  const int e = threadIdx.x;
+  if (e < E) {
+    int64_t v;
+    if (counts) {
+      const int64_t cnt = max(counts[e], 0);
+      v = (static_cast<int64_t>(num) * cnt + den - 1) / den;
+    } else {
+      v = (static_cast<int64_t>(num) * T * k + static_cast<int64_t>(den) * E - 1) /
+          (static_cast<int64_t>(den) * E);
+    }
+    v = max(v, static_cast<int64_t>(cap_min));
+    v = min(v, static_cast<int64_t>(T));
+    c[e] = v;
+    capacity[e] = static_cast<int32_t>(v);
+  }
+  __syncthreads();
+  if (e == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < E; ++i) {
+      offsets[i] = static_cast<int32_t>(run);
+      run += c[i];
+    }
+    offsets[E] = static_cast<int32_t>(run);
+  }
+}
+
+// Dispatch step 1: chunk histograms; also initialises src[] to -1.
+__global__ __launch_bounds__(256) void route_hist_kernel(
+    const int32_t* __restrict__ ids, int T, int E, int k, int nblk, int64_t rows_alloc,
+    int32_t* __restrict__ hist, int32_t* __restrict__ src, int32_t* status) {
+  __shared__ int h[kMaxE];
+  if (threadIdx.x < kMaxE) h[threadIdx.x] = 0;
+  const int64_t rs = (rows_alloc + nblk - 1) / nblk;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rs;
+  const int64_t r1 = min(rows_alloc, r0 + rs);
+  for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) src[r] = -1;
+  __syncthreads();
+  const int64_t n = static_cast<int64_t>(T) * k;
+  const int64_t q0 = static_cast<int64_t>(blockIdx.x) * kChunk;
+  const int64_t q1 = min(n, q0 + kChunk);
+  for (int64_t q = q0 + threadIdx.x; q < q1; q += 256) {
+    const int j = static_cast<int>(q / T), t = static_cast<int>(q - static_cast<int64_t>(j) * T);
+    if (live_assignment(ids, t, j, k, E, status)) atomicAdd(&h[ids[static_cast<size_t>(t) * k + j]], 1);
+  }
+  __syncthreads();
+  if (threadIdx.x < E) hist[static_cast<size_t>(blockIdx.x) * E + threadIdx.x] = h[threadIdx.x];
+}
+
+// Dispatch step 2: per-expert exclusive scan over chunks, counts, the usable
+// capacity of each region, fill.
+__global__ __launch_bounds__(64) void route_scan_kernel(
+    const int32_t* __restrict__ hist, int nblk, int E, const int32_t* __restrict__ capacity,
+    const int32_t* __restrict__ offsets, int64_t rows_alloc, int32_t* __restrict__ base,
+    int32_t* __restrict__ cap_eff, int32_t* __restrict__ counts, int32_t* __restrict__ fill,
+    int32_t* status) {
+  const int e = threadIdx.x;
+  if (e >= E) return;
+  int run = 0;
+  for (int b = 0; b < nblk; ++b) {
+    base[static_cast<size_t>(b) * E + e] = run;
+    run += hist[static_cast<size_t>(b) * E + e];
+  }
+  counts[e] = run;
+  const int64_t off = offsets[e];
+  const int64_t cap = capacity[e];
+  int64_t room = 0;
+  if (off >= 0) {
+    room = cap;
+    room = min(room, static_cast<int64_t>(offsets[e + 1]) - off);
+    room = min(room, rows_alloc - off);
+    room = max(room, int64_t(0));
+  }
+  if (room < cap) atomicOr(status, MOE_STATUS_REGION);
+  cap_eff[e] = static_cast<int32_t>(room);
+  fill[e] = static_cast<int32_t>(min(static_cast<int64_t>(run), room));
+}
+
+// Dispatch step 3: rank within chunk (wavefront ballots), keep/dest/src.
+__global__ __launch_bounds__(256) void route_rank_kernel(
+    const int32_t* __restrict__ ids, int T, int E, int k, const int32_t* __restrict__ base,
+    const int32_t* __restrict__ cap_eff, const int32_t* __restrict__ offsets,
+    int32_t* __restrict__ dest_row, int32_t* __restrict__ src) {
+  __shared__ int run[kMaxE];
+  __shared__ int wcnt[4][kMaxE];
+  __shared__ int capv[kMaxE];
+  __shared__ int offv[kMaxE];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (threadIdx.x < E) {
+    run[threadIdx.x] = base[static_cast<size_t>(blockIdx.x) * E + threadIdx.x];
+    capv[threadIdx.x] = cap_eff[threadIdx.x];
+    offv[threadIdx.x] = offsets[threadIdx.x];
+  }
+  for (int i = threadIdx.x; i < 4 * kMaxE; i += 256) (&wcnt[0][0])[i] = 0;
+  __syncthreads();
+  const int64_t n = static_cast<int64_t>(T) * k;
+  const int64_t q0 = static_cast<int64_t>(blockIdx.x) * kChunk;
+  const int64_t q1 = min(n, q0 + kChunk);
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int64_t qb = q0; qb < q1; qb += 256) {
+    const int64_t q = qb + threadIdx.x;
+    int e = -1, t = 0, j = 0;
+    if (q < q1) {
+      j = static_cast<int>(q / T);
+      t = static_cast<int>(q - static_cast<int64_t>(j) * T);
+      if (live_assignment(ids, t, j, k, E, nullptr)) e = ids[static_cast<size_t>(t) * k + j];
+    }
+    const bool live = e >= 0;
+    uint64_t eq = __ballot(live);
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+      const bool bit = live && ((e >> b) & 1);
+      const uint64_t m = __ballot(bit);
+      eq &= bit ? m : ~m;
+    }
+    int rank = 0;
+    if (live) {
+      rank = __popcll(eq & lt_mask);
+      if (rank == 0) wcnt[wave][e] = __popcll(eq);
+    }
+    __syncthreads();
+    if (live) {
+      int pos = run[e] + rank;
+      for (int w = 0; w < wave; ++w) pos += wcnt[w][e];
+      const size_t a = static_cast<size_t>(t) * k + j;
+      if (pos < capv[e]) {
+        const int r = offv[e] + pos;
+        dest_row[a] = r;
+        src[r] = static_cast<int32_t>(a);
+      } else {
+        dest_row[a] = -1;
+      }
+    } else if (q < q1) {
+      dest_row[static_cast<size_t>(t) * k + j] = -1;
+    }
+    __syncthreads();
+    if (threadIdx.x < E) {
+      run[threadIdx.x] += wcnt[0][threadIdx.x] + wcnt[1][threadIdx.x] +
+                          wcnt[2][threadIdx.x] + wcnt[3][threadIdx.x];
+      wcnt[0][threadIdx.x] = wcnt[1][threadIdx.x] = 0;
+      wcnt[2][threadIdx.x] = wcnt[3][threadIdx.x] = 0;
+    }
+    __syncthreads();
+  }
+}
+
+// Token-major row kernels: one wavefront per token, `nvec` 16-byte vectors
+// per row (row bytes / 16), lanes stride over the row.
+constexpr int kRowWaves = 4;
+
+// Dispatch step 4: x_disp[dest_row[t,j]] = x[t] for every kept j.
+__global__ __launch_bounds__(256) void gather_rows_kernel(
+    const uint4* __restrict__ x, const int32_t* __restrict__ dest_row, int T, int k,
+    int nvec, uint4* __restrict__ x_disp) {
+  const int t = blockIdx.x * kRowWaves + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= T) return;
+  int dst[kMaxK];
+  bool any = false;
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    dst[j] = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
+    any |= dst[j] >= 0;
+  }
+  if (!any) return;
+  const uint4* xr = x + static_cast<size_t>(t) * nvec;
+  for (int v = lane; v < nvec; v += 64) {
+    const uint4 val = xr[v];
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+      if (dst[j] >= 0) x_disp[static_cast<size_t>(dst[j]) * nvec + v] = val;
+  }
+}
+
+// y[t] = sum_j kept w[t,j] * y_disp[dest_row[t,j]]  (fp32 sum in order j)
+template <typename T>
+__global__ __launch_bounds__(256) void combine_kernel(
+    const uint4* __restrict__ yd, const int32_t* __restrict__ dest_row,
+    const float* __restrict__ wts, int Ttok, int k, int nvec, int64_t rows_alloc,
+    uint4* __restrict__ y) {
+  constexpr int V = Elem<T>::kVec;
+  const int t = blockIdx.x * kRowWaves + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= Ttok) return;
+  int dst[kMaxK];
+  float w[kMaxK];
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    dst[j] = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
+    if (dst[j] >= rows_alloc) dst[j] = -1;  // not a row of y_disp: treated as dropped
+    w[j] = j < k ? wts[static_cast<size_t>(t) * k + j] : 0.f;
+  }
+  uint4* yr = y + static_cast<size_t>(t) * nvec;
+  for (int v = lane; v < nvec; v += 64) {
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+      if (dst[j] >= 0) {
+        float f[V];
+        Elem<T>::load(yd[static_cast<size_t>(dst[j]) * nvec + v], f);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = fmaf(w[j], f[i], acc[i]);
+      }
+    }
+    yr[v] = Elem<T>::store(acc);
+  }
+}
+
+// dweights[t,j] = <dy[t], y_disp[r]>; dy_disp[r] = w[t,j] * dy[t]
+template <typename T>
+__global__ __launch_bounds__(256) void combine_bwd_kernel(
+    const uint4* __restrict__ dy, const uint4* __restrict__ yd,
+    const int32_t* __restrict__ dest_row, const float* __restrict__ wts, int Ttok, int k,
+    int nvec, int64_t rows_alloc, uint4* __restrict__ dyd, float* __restrict__ dweights) {
+  constexpr int V = Elem<T>::kVec;
+  const int t = blockIdx.x * kRowWaves + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= Ttok) return;
+  int dst[kMaxK];
+  float w[kMaxK], dot[kMaxK];
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    dst[j] = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
+    if (dst[j] >= rows_alloc) dst[j] = -1;  // not a row of the grouped buffers
+    w[j] = j < k ? wts[static_cast<size_t>(t) * k + j] : 0.f;
+    dot[j] = 0.f;
+  }
+  const uint4* dr = dy + static_cast<size_t>(t) * nvec;
+  for (int v = lane; v < nvec; v += 64) {
+    float g[V];
+    Elem<T>::load(dr[v], g);
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+      if (dst[j] >= 0) {
+        float f[V], o[V];
+        const size_t ro = static_cast<size_t>(dst[j]) * nvec + v;
+        Elem<T>::load(yd[ro], f);
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+          dot[j] = fmaf(g[i], f[i], dot[j]);
+          o[i] = w[j] * g[i];
+        }
+        dyd[ro] = Elem<T>::store(o);
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    if (j < k) {
+      const float s = wave_sum(dot[j]);
+      if (lane == 0) dweights[static_cast<size_t>(t) * k + j] = dst[j] >= 0 ? s : 0.f;
+    }
+  }
+}
+
+// dx[t] = sum_j kept dx_disp[r_j] (+ dl[t] . w_g).  Tokens are processed
+// kTokGroup at a time per wavefront so each w_g vector is loaded once per
+// group rather than once per token.
+constexpr int kTokGroup = 4;
+
+template <typename T, bool GATE>
+__global__ __launch_bounds__(256) void dispatch_bwd_kernel(
+    const uint4* __restrict__ dxd, const int32_t* __restrict__ dest_row,
+    const float* __restrict__ dl, const uint4* __restrict__ wg, int Ttok, int E, int k,
+    int nvec, int64_t rows_alloc, uint4* __restrict__ dx) {
+  constexpr int V = Elem<T>::kVec;
+  const int tg = (blockIdx.x * kRowWaves + (threadIdx.x >> 6)) * kTokGroup;
+  const int lane = threadIdx.x & 63;
+  if (tg >= Ttok) return;
+  for (int v = lane; v < nvec; v += 64) {
+    float acc[kTokGroup][V];
+#pragma unroll
+    for (int u = 0; u < kTokGroup; ++u) {
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[u][i] = 0.f;
+      const int t = tg + u;
+      if (t >= Ttok) continue;
+      for (int j = 0; j < k; ++j) {
+        const int r = dest_row[static_cast<size_t>(t) * k + j];
+        if (r >= 0 && r < rows_alloc) {
+          float f[V];
+          Elem<T>::load(dxd[static_cast<size_t>(r) * nvec + v], f);
+#pragma unroll
+          for (int i = 0; i < V; ++i) acc[u][i] += f[i];
+        }
+      }
+    }
+    if constexpr (GATE) {
+      for (int e = 0; e < E; ++e) {
+        float f[V];
+        Elem<T>::load(wg[static_cast<size_t>(e) * nvec + v], f);
+#pragma unroll
+        for (int u = 0; u < kTokGroup; ++u) {
+          const int t = tg + u;
+          const float g = t < Ttok ? dl[static_cast<size_t>(t) * E + e] : 0.f;
+#pragma unroll
+          for (int i = 0; i < V; ++i) acc[u][i] = fmaf(g, f[i], acc[u][i]);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kTokGroup; ++u)
+      if (tg + u < Ttok) dx[static_cast<size_t>(tg + u) * nvec + v] = Elem<T>::store(acc[u]);
+  }
+}
+
+inline int nblocks(int64_t n, int per) { return static_cast<int>((n + per - 1) / per); }
+
+}  // namespace
+}  // namespace moe
+
+using namespace moe;
+
+extern "C" moe_status moe_count(void* stream, int T, int E, int k, const int32_t* ids,
+                                int32_t* counts, int32_t* status) {
+  if (!shape_ok(T, E, k) || !counts || !status) return MOE_EINVAL;
+  if (T > 0 && !ids) return MOE_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  fill_i32_kernel<<<1, 64, 0, s>>>(counts, E, 0);
+  MOE_LAUNCH_CHECK();
+  const int64_t n = static_cast<int64_t>(T) * k;
+  if (n > 0) {
+    count_kernel<<<nblocks(n, kChunk), 256, 0, s>>>(ids, T, E, k, counts, status);
+    MOE_LAUNCH_CHECK();
+  }
+  return MOE_OK;
+}
+
+extern "C" moe_status moe_update_capacity(void* stream, int T, int k, int E,
+                                          const int32_t* counts, int num, int den,
+                                          int cap_min, int32_t* capacity, int32_t* offsets) {
+  if (!shape_ok(T, E, k) || num < 1 || den < 1 || cap_min < 0) return MOE_EINVAL;
+  if (!capacity || !offsets) return MOE_EINVAL;
+  if (static_cast<int64_t>(T) * E >= (int64_t(1) << 31)) return MOE_EINVAL;
+  capacity_kernel<<<1, 64, 0, static_cast<hipStream_t>(stream)>>>(T, k, E, counts, num, den,
+                                                                 cap_min, capacity, offsets);
+  MOE_LAUNCH_CHECK();
+  return MOE_OK;
+}
+
+static int route_nblk(int T, int k) {
+  const int64_t n = static_cast<int64_t>(T) * k;
+  return n > 0 ? nblocks(n, kChunk) : 1;
+}
+
+extern "C" size_t moe_dispatch_workspace_bytes(int T, int E, int k) {
+  if (!shape_ok(T, E, k)) return 0;
+  const size_t nblk = route_nblk(T, k);
+  return align_up((2 * nblk * E + E) * sizeof(int32_t), 256);
+}
+
+extern "C" moe_status moe_dispatch(void* stream, moe_dtype dt, int T, int d, int E, int k,
+                                   const void* x, const int32_t* ids,
+                                   const int32_t* capacity, const int32_t* offsets,
+                                   int64_t rows_alloc, int32_t* counts, int32_t* fill,
+                                   int32_t* dest_row, int32_t* src, void* x_disp,
+                                   int32_t* status, void* workspace, size_t workspace_bytes) {
+  if (!dtype_ok(dt) || !shape_ok(T, E, k) || !width_ok(d) || !rows_ok(rows_alloc))
+    return MOE_EINVAL;
+  if (!capacity || !offsets || !counts || !fill || !status) return MOE_EINVAL;
+  if (rows_alloc > 0 && (!src || !x_disp)) return MOE_EINVAL;
+  if (T > 0 && (!x || !ids || !dest_row)) return MOE_EINVAL;
+  if ((x && !aligned16(x)) || (x_disp && !aligned16(x_disp))) return MOE_EINVAL;
+  const size_t need = moe_dispatch_workspace_bytes(T, E, k);
+  if (!workspace || workspace_bytes < need) return MOE_EWORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nblk = route_nblk(T, k);
+  int32_t* hist = static_cast<int32_t*>(workspace);
+  int32_t* base = hist + static_cast<size_t>(nblk) * E;
+  int32_t* cap_eff = base + static_cast<size_t>(nblk) * E;
+  route_hist_kernel<<<nblk, 256, 0, s>>>(ids, T, E, k, nblk, rows_alloc, hist, src, status);
+  MOE_LAUNCH_CHECK();
+  route_scan_kernel<<<1, 64, 0, s>>>(hist, nblk, E, capacity, offsets, rows_alloc, base,
+                                     cap_eff, counts, fill, status);
+  MOE_LAUNCH_CHECK();
+  if (T == 0) return MOE_OK;
+  route_rank_kernel<<<nblk, 256, 0, s>>>(ids, T, E, k, base, cap_eff, offsets, dest_row, src);
+  MOE_LAUNCH_CHECK();
+  const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
+  gather_rows_kernel<<<nblocks(T, kRowWaves), 256, 0, s>>>(
+      static_cast<const uint4*>(x), dest_row, T, k, nvec, static_cast<uint4*>(x_disp));
+  MOE_LAUNCH_CHECK();
+  return MOE_OK;
+}
+
+extern "C" moe_status moe_combine(void* stream, moe_dtype dt, int T, int d, int k,
+                                  int64_t rows_alloc, const void* y_disp,
+                                  const int32_t* dest_row, const float* weights, void* y) {
+  if (!dtype_ok(dt) || T < 0 || k < 1 || k > kMaxK || !width_ok(d) || !rows_ok(rows_alloc))
+    return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!y_disp || !dest_row || !weights || !y) return MOE_EINVAL;
+  if (!aligned16(y_disp) || !aligned16(y)) return MOE_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
+  if (dt == MOE_BF16)
+    combine_kernel<uint16_t><<<nblocks(T, kRowWaves), 256, 0, s>>>(
+        static_cast<const uint4*>(y_disp), dest_row, weights, T, k, nvec, rows_alloc,
+        static_cast<uint4*>(y));
+  else
+    combine_kernel<float><<<nblocks(T, kRowWaves), 256, 0, s>>>(
+        static_cast<const uint4*>(y_disp), dest_row, weights, T, k, nvec, rows_alloc,
+        static_cast<uint4*>(y));
+  MOE_LAUNCH_CHECK();
+  return MOE_OK;
+}
+
+extern "C" moe_status moe_combine_bwd(void* stream, moe_dtype dt, int T, int d, int k,
+                                      int64_t rows_alloc, const void* dy, const void* y_disp,
+                                      const int32_t* dest_row, const float* weights,
+                                      void* dy_disp, float* dweights) {
+  if (!dtype_ok(dt) || T < 0 || k < 1 || k > kMaxK || !width_ok(d) || !rows_ok(rows_alloc))
+    return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!dy || !y_disp || !dest_row || !weights || !dy_disp || !dweights) return MOE_EINVAL;
+  if (!aligned16(dy) || !aligned16(y_disp) || !aligned16(dy_disp)) return MOE_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
+  if (dt == MOE_BF16)
+    combine_bwd_kernel<uint16_t><<<nblocks(T, kRowWaves), 256, 0, s>>>(
+        static_cast<const uint4*>(dy), static_cast<const uint4*>(y_disp), dest_row, weights, T,
+        k, nvec, rows_alloc, static_cast<uint4*>(dy_disp), dweights);
+  else
+    combine_bwd_kernel<float><<<nblocks(T, kRowWaves), 256, 0, s>>>(
+        static_cast<const uint4*>(dy), static_cast<const uint4*>(y_disp), dest_row, weights, T,
+        k, nvec, rows_alloc, static_cast<uint4*>(dy_disp), dweights);
+  MOE_LAUNCH_CHECK();
+  return MOE_OK;
+}
+
+extern "C" moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d, int E, int k,
+                                       int64_t rows_alloc, const void* dx_disp,
+                                       const int32_t* dest_row, const float* dlogits,
+                                       const void* w_g, void* dx) {
+  if (!dtype_ok(dt) || !shape_ok(T, E, k) || !width_ok(d) || !rows_ok(rows_alloc))
+    return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!dx_disp || !dest_row || !dx) return MOE_EINVAL;
+  if ((dlogits == nullptr) != (w_g == nullptr)) return MOE_EINVAL;
+  if (!aligned16(dx_disp) || !aligned16(dx) || (w_g && !aligned16(w_g))) return MOE_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
+  const int grid = nblocks(T, kRowWaves * kTokGroup);
+  const uint4* a = static_cast<const uint4*>(dx_disp);
+  const uint4* g = static_cast<const uint4*>(w_g);
+  uint4* o = static_cast<uint4*>(dx);
+  if (dt == MOE_BF16) {
+    if (dlogits)
+      dispatch_bwd_kernel<uint16_t, true><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
+    else
+      dispatch_bwd_kernel<uint16_t, false><<<grid, 256, 0, s>>>(a, dest_row, nullptr, nullptr, T, E, k, nvec, rows_alloc, o);
+  } else {
+    if (dlogits)
+      dispatch_bwd_kernel<float, true><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
+    else
+      dispatch_bwd_kernel<float, false><<<grid, 256, 0, s>>>(a, dest_row, nullptr, nullptr, T, E, k, nvec, rows_alloc, o);
+  }
+  MOE_LAUNCH_CHECK();
+  return MOE_OK;
+}

@@ -1,0 +1,166 @@
+"""One MoE layer on one GPU: device buffers plus the sequence of libmoe calls.
+
+PyTorch only allocates device memory and provides the stream; every step of
+the layer is a libmoe entry point (see include/moe.h).  Buffers are sized
+once, on the host, with no device synchronisation:
+
+* static capacity factor alpha = num/den:  rows_alloc = E * min(T, ceil(alpha*T*k/E))
+* dynamic capacity with margin num/den:    rows_alloc = min(E*T, ceil(num*T*k/den) + E)
+* exact capacity (margin 1):               rows_alloc = T*k
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import torch
+
+from . import binding as B
+
+
+def _cdiv(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+def rows_alloc_for(kind: str, T: int, k: int, E: int, num: int = 1, den: int = 1) -> int:
+    if kind == "static":
+        return E * min(T, _cdiv(num * T * k, den * E))
+    if kind == "dynamic":
+        return min(E * T, _cdiv(num * T * k, den) + E)
+    if kind == "exact":
+        return T * k
+    raise ValueError(kind)
+
+
+class MoELayer:
+    def __init__(self, T: int, d: int, E: int, k: int, f: int, act: str,
+                 dtype: torch.dtype, rows_alloc: int, backward: bool = False,
+                 gate: bool = True, device="cuda"):
+        self.T, self.d, self.E, self.k, self.f = T, d, E, k, f
+        self.act = B.ACTS[act]
+        self.swiglu = act == "swiglu"
+        self.dtype = dtype
+        self.rows_alloc = int(rows_alloc)
+        self.dev = torch.device(device)
+        self.has_gate = gate
+        dt = B.MOE_BF16 if dtype == torch.bfloat16 else B.MOE_F32
+        i32, f32 = torch.int32, torch.float32
+        e = lambda *s, t=dtype: torch.empty(*s, dtype=t, device=self.dev)
+        R = self.rows_alloc
+        self.logits = e(T, E, t=f32)
+        self.ids = e(T, k, t=i32)
+        self.weights = e(T, k, t=f32)
+        self.counts = e(E, t=i32)
+        self.fill = e(E, t=i32)
+        self.capacity = e(E, t=i32)
+        self.offsets = e(E + 1, t=i32)
+        self.status = torch.zeros(1, dtype=i32, device=self.dev)
+        self.dest_row = e(T, k, t=i32)
+        self.src = e(max(R, 1), t=i32)
+        self.x_disp = e(max(R, 1), d)
+        self.y_disp = e(max(R, 1), d)
+        self.y = e(T, d)
+        self.ws_dispatch = B.workspace(B.moe_dispatch_workspace_bytes(T, E, k), self.dev)
+        self.ws_fwd = B.workspace(B.moe_ffn_fwd_workspace_bytes(dt, self.act, E, d, f, R), self.dev)
+        self.backward_enabled = backward
+        self.h_save = None
+        if backward:
+            self.h_save = e((2 if self.swiglu else 1) * max(R, 1) * f)
+            self.dy_disp = e(max(R, 1), d)
+            self.dx_disp = e(max(R, 1), d)
+            self.dweights = e(T, k, t=f32)
+            self.dw1 = e(E, f, d, t=f32)
+            self.dw3 = e(E, f, d, t=f32) if self.swiglu else None
+            self.dw2 = e(E, d, f, t=f32)
+            self.dx = e(T, d)
+            self.ws_bwd = B.workspace(B.moe_ffn_bwd_workspace_bytes(dt, self.act, E, d, f, R),
+                                      self.dev)
+            if gate:
+                self.dlogits = e(T, E, t=f32)
+                self.dw_g = e(E, d, t=f32)
+                self.ws_gate_bwd = B.workspace(B.moe_gate_bwd_workspace_bytes(T, d, E), self.dev)
+
+    # ---- forward pieces ------------------------------------------------------
+    def gate(self, x, w_g, bias, renorm: int):
+        B.moe_gate_topk(x, w_g, bias, self.k, renorm, self.logits, self.ids, self.weights)
+
+    def count(self, ids: Optional[torch.Tensor] = None):
+        B.moe_count(self.ids if ids is None else ids, self.E, self.counts, self.status)
+
+    def capacity_static(self, num: int, den: int, cap_min: int = 0):
+        B.moe_update_capacity(self.T, self.k, self.E, None, num, den, cap_min, self.capacity,
+                              self.offsets)
+
+    def capacity_dynamic(self, num: int, den: int, counts: Optional[torch.Tensor] = None,
+                         cap_min: int = 0):
+        B.moe_update_capacity(self.T, self.k, self.E, self.counts if counts is None else counts,
+                              num, den, cap_min, self.capacity, self.offsets)
+
+    def dispatch(self, x, ids: Optional[torch.Tensor] = None):
+        B.moe_dispatch(x, self.ids if ids is None else ids, self.E, self.capacity, self.offsets,
+                       self.rows_alloc, self.counts, self.fill, self.dest_row, self.src,
+                       self.x_disp, self.status, self.ws_dispatch)
+
+    def ffn_fwd(self, w1, w3, w2, rows: str = "fill"):
+        r = self.fill if rows == "fill" else self.capacity
+        B.moe_expert_ffn_fwd(self.act, self.offsets, r, self.x_disp, w1, w3, w2, self.h_save,
+                             self.y_disp, self.ws_fwd)
+
+    def combine(self, weights: Optional[torch.Tensor] = None):
+        B.moe_combine(self.y_disp, self.dest_row, self.weights if weights is None else weights,
+                      self.y)
+
+    # ---- backward pieces -----------------------------------------------------
+    def combine_bwd(self, dy, weights: Optional[torch.Tensor] = None):
+        B.moe_combine_bwd(dy, self.y_disp, self.dest_row,
+                          self.weights if weights is None else weights, self.dy_disp,
+                          self.dweights)
+
+    def ffn_bwd(self, w1, w3, w2, rows: str = "fill"):
+        r = self.fill if rows == "fill" else self.capacity
+        B.moe_expert_ffn_bwd(self.act, self.offsets, r, self.x_disp, self.h_save, w1, w3, w2,
+                             self.dy_disp, self.dx_disp, self.dw1, self.dw3, self.dw2,
+                             self.ws_bwd)
+
+    def gate_bwd(self, x, renorm: int, ids: Optional[torch.Tensor] = None):
+        B.moe_gate_bwd(x, self.logits, self.ids if ids is None else ids, self.dweights, renorm,
+                       self.dlogits, self.dw_g, self.ws_gate_bwd)
+
+    def dispatch_bwd(self, w_g=None):
+        if w_g is not None:
+            B.moe_dispatch_bwd(self.dx_disp, self.dest_row, self.E, self.dlogits, w_g, self.dx)
+        else:
+            B.moe_dispatch_bwd(self.dx_disp, self.dest_row, self.E, None, None, self.dx)
+
+    # ---- whole layer ---------------------------------------------------------
+    def forward(self, x, w1, w3, w2, *, w_g=None, bias=None, renorm=0, ids=None, weights=None,
+                capacity=("dynamic", 1, 1), counts_from_batch=True, rows="fill"):
+        """gate (or cached ids) -> [count ->] capacity -> dispatch -> FFN -> combine.
+
+        capacity = ("static", num, den) | ("dynamic", num, den); a dynamic rule
+        uses this batch's counts when counts_from_batch, else the counts left
+        in self.counts by the previous dispatch (a lagged capacity update)."""
+        if ids is None:
+            self.gate(x, w_g, bias, renorm)
+            ids, weights = self.ids, self.weights
+        kind, num, den = capacity
+        if kind == "static":
+            self.capacity_static(num, den)
+        else:
+            if counts_from_batch:
+                self.count(ids)
+            self.capacity_dynamic(num, den)
+        self.dispatch(x, ids)
+        self.ffn_fwd(w1, w3, w2, rows=rows)
+        self.combine(weights)
+        return self.y
+
+    def backward(self, x, dy, w1, w3, w2, *, w_g=None, renorm=0, ids=None, weights=None,
+                 rows="fill"):
+        self.combine_bwd(dy, self.weights if weights is None else weights)
+        self.ffn_bwd(w1, w3, w2, rows=rows)
+        if w_g is not None:
+            self.gate_bwd(x, renorm, ids)
+            self.dispatch_bwd(w_g)
+        else:
+            self.dispatch_bwd(None)
+        return self.dx

@@ -1,0 +1,116 @@
+"""The C ABI without a GPU: libmoe.so loads, exports every function that
+include/moe.h declares, and rejects bad arguments synchronously (these calls
+return before any device work is enqueued)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2205_01848_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+EINVAL, EWORKSPACE = 1, 4
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ["moe_gate_topk", "moe_dispatch", "moe_update_capacity", "moe_expert_ffn_fwd",
+                     "moe_expert_ffn_bwd", "moe_combine", "moe_combine_bwd", "moe_gate_bwd",
+                     "moe_dispatch_bwd", "moe_count"]:
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert name in B.SIGNATURES, f"binding lacks {name}"
+    assert lib.moe_abi_version() == 1
+    assert lib.moe_status_string(0) == b"MOE_OK"
+
+
+FAKE = ctypes.c_void_p(1 << 20)   # never dereferenced: every call below fails validation
+
+
+@pytest.mark.parametrize("args", [
+    (1, -1, 64, 4, 1, 0),      # T < 0
+    (1, 16, 60, 4, 1, 0),      # d not a multiple of 8
+    (1, 16, 64, 65, 1, 0),     # E > 64
+    (1, 16, 64, 4, 5, 0),      # k > E
+    (1, 16, 64, 16, 9, 0),     # k > 8
+    (7, 16, 64, 4, 1, 0),      # bad dtype
+])
+def test_gate_rejects_bad_shapes(args):
+    dt, T, d, E, k, renorm = args
+    L = B.lib()
+    st = L.moe_gate_topk(None, dt, T, d, E, k, renorm, FAKE, FAKE, None, FAKE, FAKE, FAKE)
+    assert st == EINVAL
+
+
+def test_gate_rejects_null_and_misaligned():
+    L = B.lib()
+    assert L.moe_gate_topk(None, 1, 16, 64, 4, 1, 0, None, FAKE, None, FAKE, FAKE, FAKE) == EINVAL
+    odd = ctypes.c_void_p((1 << 20) + 2)
+    assert L.moe_gate_topk(None, 1, 16, 64, 4, 1, 0, odd, FAKE, None, FAKE, FAKE, FAKE) == EINVAL
+
+
+def test_capacity_and_count_reject_bad_arguments():
+    L = B.lib()
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 0, 1, 0, FAKE, FAKE) == EINVAL   # num < 1
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 0, 0, FAKE, FAKE) == EINVAL   # den < 1
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 1, -1, FAKE, FAKE) == EINVAL  # cap_min
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 1, 0, None, FAKE) == EINVAL
+    assert L.moe_count(None, 10, 4, 1, FAKE, None, FAKE) == EINVAL
+
+
+def test_dispatch_workspace_and_arguments():
+    L = B.lib()
+    need = L.moe_dispatch_workspace_bytes(1000, 8, 2)
+    assert need > 0
+    assert L.moe_dispatch_workspace_bytes(1000, 8, 9) == 0
+    args = [None, 1, 1000, 64, 8, 2, FAKE, FAKE, FAKE, FAKE, 2000, FAKE, FAKE, FAKE, FAKE, FAKE,
+            FAKE]
+    assert L.moe_dispatch(*args, FAKE, need - 1) == EWORKSPACE
+    assert L.moe_dispatch(*args, None, need) == EWORKSPACE
+    bad_rows = list(args)
+    bad_rows[10] = -5
+    assert L.moe_dispatch(*bad_rows, FAKE, need) == EINVAL
+
+
+def test_ffn_workspace_queries_and_arguments():
+    L = B.lib()
+    for act in (0, 1, 2):
+        fw = L.moe_ffn_fwd_workspace_bytes(1, act, 8, 256, 512, 5000)
+        bw = L.moe_ffn_bwd_workspace_bytes(1, act, 8, 256, 512, 5000)
+        assert 0 < fw < bw
+    assert L.moe_ffn_fwd_workspace_bytes(1, 3, 8, 256, 512, 5000) == 0          # bad act
+    assert L.moe_ffn_fwd_workspace_bytes(1, 0, 8, 250, 512, 5000) == 0          # d % 8
+    need = L.moe_ffn_fwd_workspace_bytes(1, 2, 8, 256, 512, 5000)
+    base = [None, 1, 2, 8, 256, 512, FAKE, FAKE, 5000, FAKE, FAKE]
+    # SwiGLU without w3
+    assert L.moe_expert_ffn_fwd(*base, None, FAKE, None, FAKE, FAKE, need) == EINVAL
+    assert L.moe_expert_ffn_fwd(*base, FAKE, FAKE, None, FAKE, FAKE, need - 1) == EWORKSPACE
+    needb = L.moe_ffn_bwd_workspace_bytes(1, 0, 8, 256, 512, 5000)
+    assert L.moe_expert_ffn_bwd(None, 1, 0, 8, 256, 512, FAKE, FAKE, 5000, FAKE, FAKE, FAKE, None,
+                                FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, needb - 1) == EWORKSPACE
+
+
+def test_combine_and_backward_reject_bad_arguments():
+    L = B.lib()
+    assert L.moe_combine(None, 1, 10, 64, 0, 100, FAKE, FAKE, FAKE, FAKE) == EINVAL      # k = 0
+    assert L.moe_combine_bwd(None, 1, 10, 64, 2, 100, None, FAKE, FAKE, FAKE, FAKE,
+                             FAKE) == EINVAL
+    # dlogits without w_g
+    assert L.moe_dispatch_bwd(None, 1, 10, 64, 4, 2, 100, FAKE, FAKE, FAKE, None, FAKE) == EINVAL
+    assert L.moe_gate_bwd_workspace_bytes(100, 64, 4) > 0
+    assert L.moe_gate_bwd(None, 1, 100, 64, 4, 2, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                          0) == EWORKSPACE
