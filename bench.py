@@ -1,0 +1,264 @@
+"""Benchmark of one MoE layer step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c5]
+
+A step is one pass of the whole layer over one batch of synthetic inputs:
+gate + top-k (or cached ids) -> per-expert load count -> capacity update ->
+dispatch -> expert FFN -> combine, and for training workloads the backward
+(combine, FFN, gate, dispatch).  Inputs are resident in HBM before timing.
+Prints ONE JSON line.  Per-kernel times come from HIP events that libmoe
+records around each of its launches during the timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE layer tokens/sec fwd(+bwd) on 1 MI355X; % MFMA peak (GEMM), % HBM BW (dispatch)"
+PEAK_BF16_TFLOPS = 2516.6    # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 flop/clk)
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+DESCR = {
+    "c1": "T=256 d=64 E=4 top-1 d_ff=128 ReLU fp32, static capacity 1.25, forward",
+    "c2": "T=8192 d=512 E=16 top-2 d_ff=2048 GELU-tanh bf16, dynamic capacity 1.1, forward",
+    "c3": "T=16384 d=1024 E=64 top-1 d_ff=4096 ReLU bf16 Zipf gate bias, dynamic capacity 1.1, forward+backward",
+    "c4": "T=32768 d=2048 E=32 top-2 d_ff=8192 ReLU bf16 cached Zipf(1.2) assignments, exact capacity, forward+backward",
+    "c5": "T=65536 d=4096 E=8 top-2 d_ff=14336 SwiGLU bf16, dynamic capacity 1.05, forward+backward",
+}
+# bounded oracle sample (tokens) per workload, about 10-30 s of CPU work
+CPU_SAMPLE = {"c1": 256, "c2": 8192, "c3": 16384, "c4": 2048, "c5": 512}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="c5", choices=sorted(DESCR))
+    ap.add_argument("--capacity", default=None,
+                    help="override: static:num/den or dynamic:num/den")
+    ap.add_argument("--rows", default="fill", choices=["fill", "capacity"],
+                    help="capacity = padded static-shape baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def gemm_flops(wl, kept):
+    """Algorithmic MFMA flops per GEMM pass over `kept` rows."""
+    unit = 2 * kept * wl.d * wl.f
+    g = 2 if wl.act == "swiglu" else 1
+    fl = {"gemm_fwd_h": g * unit, "gemm_fwd_y": unit}
+    if wl.backward:
+        fl.update({"gemm_bwd_da": unit, "gemm_bwd_dx": g * unit, "gemm_bwd_dw2": unit,
+                   "gemm_bwd_dw13": g * unit})
+    return fl
+
+
+def hbm_bytes(wl, kept, active):
+    """Algorithmic HBM bytes per launch of the row-moving kernels."""
+    s, T, d, E, k = wl.esize, wl.T, wl.d, wl.E, wl.k
+    b = {
+        "gate_fwd": T * d * s + E * d * s + T * E * 4 + T * k * 8,
+        "dispatch_gather": active * d * s + kept * d * s + T * k * 4,
+        "combine": kept * d * s + T * d * s + T * k * 8,
+    }
+    if wl.backward:
+        b["combine_bwd"] = T * d * s + 2 * kept * d * s + T * k * 12
+        b["dispatch_bwd"] = kept * d * s + T * d * s + T * k * 4 + \
+            (T * E * 4 + E * d * s if wl.gate == "linear" else 0)
+    if wl.gate != "linear":
+        del b["gate_fwd"]
+    return b
+
+
+def cpu_baseline(wl, I, cap_rule, ntok):
+    """The oracle as it stands, on the first `ntok` tokens of the batch (the
+    same per-token work: gate, capacity on the sample's own counts,
+    dispatch, FFN, combine, backward)."""
+    import numpy as np
+    import threadpoolctl
+
+    import oracle as O
+    f64 = O.bf16_to_f64 if wl.dtype == "bf16" else (lambda a: np.asarray(a, np.float64))
+    X = f64(I.x[:ntok])
+    W1, W2 = f64(I.w1), f64(I.w2)
+    W3 = f64(I.w3) if I.w3 is not None else None
+    WG = f64(I.w_g) if I.w_g is not None else None
+    dY = f64(I.dy[:ntok]) if I.dy is not None else None
+    kind, num, den = cap_rule
+    t0 = time.perf_counter()
+    if wl.gate == "linear":
+        r = O.route(X, WG, I.bias, wl.k, wl.renorm)
+        ids, wts, logits = r["ids"], r["weights"], r["logits"]
+    else:
+        ids, wts, logits = I.ids[:ntok], I.cw[:ntok].astype(np.float64), None
+    counts = O.count_assignments(ids, wl.E)
+    if kind == "static":
+        cap = O.capacity_static(ntok, wl.k, wl.E, num, den)
+    else:
+        cap = O.capacity_dynamic(counts, ntok, num, den)
+    R = int(cap.sum())
+    fw = O.layer_forward(X, W1, W3, W2, wl.act, wl.dtype, ids, wts, cap, R, wl.E)
+    if wl.backward:
+        O.layer_backward(fw, X, dY, W1, W3, W2, wl.act, wl.dtype, ids, wts, wl.E,
+                         logits=logits, renorm=wl.renorm, w_g=WG)
+    el = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()] + [1])
+    return {"value": ntok / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {ntok} of {wl.T} tokens of the workload, "
+                      f"{'forward+backward' if wl.backward else 'forward'}, float64 numpy "
+                      f"({el:.1f} s)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer is not "
+              "sharded across GPUs in this build.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2205_01848_amd import MoELayer, binding as B, rows_alloc_for
+
+    wl = W.config(args.workload)
+    cap_rule = wl.capacity[-1]
+    if args.capacity:
+        kind, frac = args.capacity.split(":")
+        num, den = (int(v) for v in frac.split("/"))
+        cap_rule = (kind, num, den)
+    dev = torch.device("cuda:0")
+    log(f"workload {args.workload}: generating inputs")
+    t_gen = time.perf_counter()
+    I = W.make_inputs(wl)
+    t_gen = time.perf_counter() - t_gen
+    log(f"inputs ready in {t_gen:.1f} s; uploading")
+    td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+
+    def up(a):
+        if a is None:
+            return None
+        if wl.dtype == "bf16" and a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    x, w1, w3, w2, dy = (up(a) for a in (I.x, I.w1, I.w3, I.w2, I.dy))
+    kind, num, den = cap_rule
+    R = rows_alloc_for(kind, wl.T, wl.k, wl.E, num, den)
+    L = MoELayer(wl.T, wl.d, wl.E, wl.k, wl.f, wl.act, td, R, backward=wl.backward,
+                 gate=wl.gate == "linear")
+    if wl.gate == "linear":
+        fkw = dict(w_g=up(I.w_g), bias=None if I.bias is None else up(I.bias), renorm=wl.renorm)
+        bkw = dict(w_g=fkw["w_g"], renorm=wl.renorm)
+    else:
+        fkw = dict(ids=up(I.ids), weights=up(I.cw))
+        bkw = dict(weights=fkw["weights"])
+
+    def step():
+        L.forward(x, w1, w3, w2, capacity=cap_rule, rows=args.rows, **fkw)
+        if wl.backward:
+            L.backward(x, dy, w1, w3, w2, rows=args.rows, **bkw)
+
+    log("warmup")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("timed steps")
+    kept = int(L.fill.sum().item())
+    executed = int((L.fill if args.rows == "fill" else L.capacity).sum().item())
+    active = int((L.dest_row >= 0).any(dim=1).sum().item())
+    status = int(L.status.item())
+
+    B.moe_timing_report()            # drop warmup records
+    B.moe_timing_enable(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    B.moe_timing_enable(False)
+    total_ms = ev0.elapsed_time(ev1)
+    kern = B.moe_timing_report()
+    ms_step = total_ms / args.steps
+
+    # per-kernel rates
+    fl = gemm_flops(wl, executed)
+    fl_alg = gemm_flops(wl, kept)
+    by = hbm_bytes(wl, kept, active)
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    detail = {}
+    for name, (n, ms) in kern.items():
+        avg = ms / max(n, 1)
+        row = {"launches": n, "avg_ms": round(avg, 4), "share": round(ms / total_ms, 4)}
+        if name in fl:
+            row["tflops"] = round(fl_alg[name] / avg / 1e9, 1)
+            row["frac_mfma_peak"] = round(fl_alg[name] / avg / 1e9 / peak, 4)
+        if name in by:
+            row["gbs"] = round(by[name] / avg / 1e6, 1)
+            row["frac_hbm"] = round(by[name] / avg / 1e6 / PEAK_HBM_GBS, 4)
+        detail[name] = row
+    dom = max(kern.items(), key=lambda kv: kv[1][1])[0] if kern else None
+    roof = None
+    if dom in fl:
+        n, ms = kern[dom]
+        avg_s = ms / n / 1e3
+        ach = fl_alg[dom] / avg_s / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(ach / peak, 4), "traffic": None}
+    elif dom in by:
+        n, ms = kern[dom]
+        ach = by[dom] / (ms / n / 1e3) / 1e9
+        roof = {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+    gemm_ms = sum(kern[k][1] for k in kern if k in fl)
+    gemm_fl = sum(fl_alg[k] * kern[k][0] for k in kern if k in fl)
+
+    log(f"{ms_step:.3f} ms/step; oracle baseline")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, I, cap_rule, CPU_SAMPLE[args.workload])
+
+    out = {
+        "metric": METRIC,
+        "value": round(wl.T / (ms_step / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {DESCR[args.workload]}", "T": wl.T, "d": wl.d,
+                   "E": wl.E, "k": wl.k, "d_ff": wl.f, "act": wl.act,
+                   "capacity": f"{cap_rule[0]} {cap_rule[1]}/{cap_rule[2]}",
+                   "rows": args.rows, "pass": "fwd+bwd" if wl.backward else "fwd",
+                   "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "detail": {"kept_rows": kept, "executed_rows": executed, "status": status,
+                   "gemm_tflops": round(gemm_fl / (gemm_ms / 1e3) / 1e12, 1) if gemm_ms else None,
+                   "gemm_share": round(gemm_ms / total_ms, 4),
+                   "input_gen_s": round(t_gen, 1), "kernels": detail},
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

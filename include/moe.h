@@ -261,6 +261,18 @@ moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d, int E,
                             const int32_t* dest_row, const float* dlogits,
                             const void* w_g, void* dx);
 
+/*
+ * Kernel timing (instrumentation; not part of the method).  While enabled,
+ * every kernel the library launches is bracketed by two HIP events recorded
+ * on the stream it is launched on.  moe_timing_report waits for the recorded
+ * events, writes one line "name launches total_ms" per kernel name (in first
+ * launch order) into buf [host, len bytes, NUL-terminated, truncated to fit],
+ * clears the records and returns the number of names.  Off by default; leave
+ * it off under HIP graph capture.  [host]
+ */
+moe_status moe_timing_enable(int on);
+int moe_timing_report(char* buf, size_t len);
+
 #ifdef __cplusplus
 }
 #endif

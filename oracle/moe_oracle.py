@@ -354,7 +354,8 @@ def ffn_rows_bwd(X: np.ndarray, e_of_row: np.ndarray, H: np.ndarray,
 
     dA = dY W2;  relu/gelu: dH = dA * act'(H);
     swiglu: dH1 = dA * H3 * silu'(H1), dH3 = dA * silu(H1);
-    dW2_e = dY_e^T A_e, dW1_e = dH1_e^T X_e, dW3_e = dH3_e^T X_e (float32);
+    dW2_e = dY_e^T A_e, dW1_e = dH1_e^T X_e, dW3_e = dH3_e^T X_e (float32
+    arrays: summed in float64, rounded once);
     dX = dH1 W1 + dH3 W3 (one rounding).  An expert with no rows has dW = 0."""
     f = w1.shape[1]
     d = w2.shape[1]
@@ -362,9 +363,11 @@ def ffn_rows_bwd(X: np.ndarray, e_of_row: np.ndarray, H: np.ndarray,
     dX = np.zeros((R, d))
     dH = np.zeros((R, f))
     dH3 = np.zeros((R, f)) if act == "swiglu" else None
-    dW1 = np.zeros((E, f, d))
-    dW3 = np.zeros((E, f, d)) if act == "swiglu" else None
-    dW2 = np.zeros((E, d, f))
+    # weight gradients are float32 values: each is summed in float64 and
+    # rounded once to float32 (stored as float32 arrays)
+    dW1 = np.zeros((E, f, d), dtype=np.float32)
+    dW3 = np.zeros((E, f, d), dtype=np.float32) if act == "swiglu" else None
+    dW2 = np.zeros((E, d, f), dtype=np.float32)
     for e in np.unique(e_of_row):
         m = e_of_row == e
         Xe, dYe, h = X[m], dY[m], H[m]
@@ -375,19 +378,16 @@ def ffn_rows_bwd(X: np.ndarray, e_of_row: np.ndarray, H: np.ndarray,
             g1 = round_to(dA * h3 * act_grad(h, "silu"), dtype)
             g3 = round_to(dA * act_fwd(h, "silu"), dtype)
             dH[m], dH3[m] = g1, g3
-            dW3[e] = g3.T @ Xe
+            dW3[e] = _f32(g3.T @ Xe)
             dX[m] = round_to(g1 @ w1[e] + g3 @ w3[e], dtype)
         else:
             a = round_to(act_fwd(h, act), dtype)
             g1 = round_to(dA * act_grad(h, act), dtype)
             dH[m] = g1
             dX[m] = round_to(g1 @ w1[e], dtype)
-        dW1[e] = g1.T @ Xe
-        dW2[e] = dYe.T @ a
-    out = dict(dX=dX, dH=dH, dH3=dH3, dW1=_f32(dW1).astype(np.float64),
-               dW2=_f32(dW2).astype(np.float64))
-    out["dW3"] = None if dW3 is None else _f32(dW3).astype(np.float64)
-    return out
+        dW1[e] = _f32(g1.T @ Xe)
+        dW2[e] = _f32(dYe.T @ a)
+    return dict(dX=dX, dH=dH, dH3=dH3, dW1=dW1, dW2=dW2, dW3=dW3)
 
 
 # ----------------------------------------------------------------------------
@@ -523,9 +523,9 @@ def layer_backward(fw, x, dy, w1, w3, w2, act, dtype, ids, weights, E,
         dx_disp[rows] = b["dX"]
         dW1, dW2, dW3 = b["dW1"], b["dW2"], b["dW3"]
     else:
-        dW1 = np.zeros((E, f, d))
-        dW2 = np.zeros((E, d, f))
-        dW3 = np.zeros((E, f, d)) if act == "swiglu" else None
+        dW1 = np.zeros((E, f, d), dtype=np.float32)
+        dW2 = np.zeros((E, d, f), dtype=np.float32)
+        dW3 = np.zeros((E, f, d), dtype=np.float32) if act == "swiglu" else None
     dl = dwg = None
     if logits is not None:
         dl, dwg = gate_bwd(logits, ids, dw, renorm, x)

@@ -48,6 +48,8 @@ SIGNATURES = {
                               _p, _p, _p, _p, _p, _c_size]),
     "moe_dispatch_bwd": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_int, _c_i64, _p,
                                   _p, _p, _p, _p]),
+    "moe_timing_enable": (_c_int, [_c_int]),
+    "moe_timing_report": (_c_int, [ctypes.c_char_p, _c_size]),
 }
 
 _lib = None
@@ -198,3 +200,19 @@ def moe_dispatch_bwd(dx_disp, dest_row, E, dlogits, w_g, dx):
     _check(lib().moe_dispatch_bwd(_stream(), _dt(dx), T, d, E, k, dx_disp.shape[0],
                                   _ptr(dx_disp), _ptr(dest_row), _ptr(dlogits), _ptr(w_g),
                                   _ptr(dx)), "moe_dispatch_bwd")
+
+
+# ---- kernel timing (instrumentation) ----------------------------------------
+def moe_timing_enable(on: bool):
+    _check(lib().moe_timing_enable(1 if on else 0), "moe_timing_enable")
+
+
+def moe_timing_report() -> dict:
+    """{kernel name: (launches, total ms)} since the last report."""
+    buf = ctypes.create_string_buffer(1 << 16)
+    lib().moe_timing_report(buf, len(buf))
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, n, ms = line.split()
+        out[name] = (int(n), float(ms))
+    return out

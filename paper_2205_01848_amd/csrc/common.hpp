@@ -80,7 +80,27 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 __device__ __forceinline__ int ceil_div_i(int a, int b) { return (a + b - 1) / b; }
 
+// ---- opt-in kernel timing (moe_timing_enable / moe_timing_report) ---------
+// While enabled, each library kernel launch is bracketed by two HIP events
+// recorded on the launch stream; the report aggregates them by kernel name.
+bool timing_enabled();
+void timing_record(const char* name, hipStream_t s, bool start);
+
+struct TimedLaunch {
+  const char* name;
+  hipStream_t s;
+  bool on;
+  TimedLaunch(const char* n, hipStream_t st) : name(n), s(st), on(timing_enabled()) {
+    if (on) timing_record(name, s, true);
+  }
+  ~TimedLaunch() {
+    if (on) timing_record(name, s, false);
+  }
+};
+
 }  // namespace moe
+
+#define MOE_TIMED(name, stream) ::moe::TimedLaunch moe_timed_scope_(name, stream)
 
 // Host-side launch check: returns MOE_EHIP from the calling entry point.
 #define MOE_LAUNCH_CHECK()                                   \

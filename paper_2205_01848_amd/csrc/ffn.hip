@@ -348,7 +348,11 @@ __device__ __forceinline__ void decode_grouped(int L, int n_mt, int n_nt, int& m
   }
 }
 
-template <typename T, int MODE>
+// PASS only names the instance (forward H, forward Y, backward dA, dX, dW2,
+// dW1/dW3), so each product is a separate kernel in traces.
+enum Pass { P_FWD_H = 0, P_FWD_Y = 1, P_BWD_DA = 2, P_BWD_DX = 3, P_BWD_DW2 = 4, P_BWD_DW13 = 5 };
+
+template <typename T, int MODE, int PASS>
 __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams p) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsBytes];
   constexpr int ES = sizeof(T);
@@ -764,6 +768,7 @@ bool make_plan(moe_dtype dt, moe_act act, int E, int d, int f, int64_t rows_allo
 
 moe_status launch_schedule(hipStream_t s, const FfnPlan& pl, const int32_t* offsets,
                            const int32_t* rows, char* ws) {
+  MOE_TIMED("ffn_schedule", s);
   schedule_kernel<<<1, 64, 0, s>>>(
       offsets, rows, pl.E, pl.rows_alloc, pl.max_mtiles, pl.max_ttiles, pl.kpad_cap,
       pl.max_segs, pl.tmn_min, pl.max_slots, reinterpret_cast<Sched*>(ws + pl.o_sched),
@@ -782,20 +787,27 @@ GemmParams base_params(const FfnPlan& pl, const int32_t* offsets, char* ws) {
   return p;
 }
 
-template <int MODE>
+const char* pass_name(int pass) {
+  static const char* names[] = {"gemm_fwd_h", "gemm_fwd_y", "gemm_bwd_da", "gemm_bwd_dx",
+                                "gemm_bwd_dw2", "gemm_bwd_dw13"};
+  return names[pass];
+}
+
+template <int MODE, int PASS>
 moe_status launch_gemm(hipStream_t s, moe_dtype dt, const GemmParams& p) {
   const int grid = persistent_grid();
+  MOE_TIMED(pass_name(PASS), s);
   if (dt == MOE_BF16)
-    ffn_gemm_kernel<uint16_t, MODE><<<grid, kThreads, 0, s>>>(p);
+    ffn_gemm_kernel<uint16_t, MODE, PASS><<<grid, kThreads, 0, s>>>(p);
   else
-    ffn_gemm_kernel<float, MODE><<<grid, kThreads, 0, s>>>(p);
+    ffn_gemm_kernel<float, MODE, PASS><<<grid, kThreads, 0, s>>>(p);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }
 
-#define MOE_TRY(x)                         \
+#define MOE_TRY(...)                       \
   do {                                     \
-    moe_status st_ = (x);                  \
+    moe_status st_ = (__VA_ARGS__);        \
     if (st_ != MOE_OK) return st_;         \
   } while (0)
 
@@ -808,6 +820,7 @@ moe_status launch_rows_transpose(hipStream_t s, moe_dtype dt, const FfnPlan& pl,
   const int2* tt = reinterpret_cast<const int2*>(ws + pl.o_ttile);
   const int64_t ld_in = static_cast<int64_t>(D) * pl.es;
   const int64_t ld_out = static_cast<int64_t>(pl.kpad_cap) * pl.es;
+  MOE_TIMED("transpose_rows", s);
   if (dt == MOE_BF16)
     rows_transpose_kernel<uint16_t, TM><<<grid, 256, 0, s>>>(
         static_cast<const char*>(in), static_cast<const char*>(in3), ld_in, D, act, offsets, sc,
@@ -823,6 +836,7 @@ moe_status launch_rows_transpose(hipStream_t s, moe_dtype dt, const FfnPlan& pl,
 moe_status launch_weight_transpose(hipStream_t s, moe_dtype dt, const void* in, int E, int R,
                                    int C, char* out, int64_t ld_out, int co, int64_t gstride) {
   dim3 grid(cdiv(C, kTT), cdiv(R, kTT), E);
+  MOE_TIMED("transpose_weights", s);
   if (dt == MOE_BF16)
     weight_transpose_kernel<uint16_t><<<grid, 256, 0, s>>>(
         static_cast<const uint16_t*>(in), R, C, reinterpret_cast<uint16_t*>(out), ld_out, co, gstride);
@@ -837,6 +851,7 @@ moe_status launch_split_reduce(hipStream_t s, const FfnPlan& pl, char* ws, int M
                                float* dwA, float* dwB, int split_row) {
   const int64_t elems = static_cast<int64_t>(M_out) * N;
   dim3 grid(cdiv(elems, 1024), pl.E);
+  MOE_TIMED("split_reduce", s);
   split_reduce_kernel<<<grid, 256, 0, s>>>(
       reinterpret_cast<const float*>(ws + pl.o_part), elems,
       reinterpret_cast<const Sched*>(ws + pl.o_sched), dwA, dwB, static_cast<int64_t>(M_out) * N,
@@ -901,10 +916,10 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   p.ldh = f * es;
   if (act == MOE_SWIGLU) {
     p.ntiles = cdiv(f, 128);
-    MOE_TRY(launch_gemm<M_FWD1_SWIGLU>(s, dt, p));
+    MOE_TRY(launch_gemm<M_FWD1_SWIGLU, P_FWD_H>(s, dt, p));
   } else {
     p.ntiles = cdiv(f, BN);
-    MOE_TRY(launch_gemm<M_FWD1>(s, dt, p));
+    MOE_TRY(launch_gemm<M_FWD1, P_FWD_H>(s, dt, p));
   }
 
   GemmParams q = base_params(pl, offsets, ws);
@@ -918,7 +933,7 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   q.ntiles = cdiv(d, BN);
   q.C = static_cast<char*>(y_disp);
   q.ldc = d * es;
-  MOE_TRY(launch_gemm<M_STORE>(s, dt, q));
+  MOE_TRY(launch_gemm<M_STORE, P_FWD_Y>(s, dt, q));
   return MOE_OK;
 }
 
@@ -982,8 +997,8 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   p.CT = dht;
   p.ldct = static_cast<int64_t>(pl.kpad_cap) * es;
   p.f = f;
-  if (sw) MOE_TRY(launch_gemm<M_BWD_DA_SWIGLU>(s, dt, p));
-  else MOE_TRY(launch_gemm<M_BWD_DA>(s, dt, p));
+  if (sw) MOE_TRY(launch_gemm<M_BWD_DA_SWIGLU, P_BWD_DA>(s, dt, p));
+  else MOE_TRY(launch_gemm<M_BWD_DA, P_BWD_DA>(s, dt, p));
 
   // dx_disp = [dH1 | dH3] [W1 | W3]
   GemmParams q = base_params(pl, offsets, ws);
@@ -997,7 +1012,7 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   q.ntiles = cdiv(d, BN);
   q.C = static_cast<char*>(dx_disp);
   q.ldc = d * es;
-  MOE_TRY(launch_gemm<M_STORE>(s, dt, q));
+  MOE_TRY(launch_gemm<M_STORE, P_BWD_DX>(s, dt, q));
 
   // K-contiguous copies of the row operands of the weight gradients
   MOE_TRY(launch_rows_transpose<T_COPY>(s, dt, pl, offsets, ws, x_disp, nullptr, d, 0, xt));
@@ -1023,7 +1038,7 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   r.split_row = d;
   r.partial = reinterpret_cast<float*>(ws + pl.o_part);
   r.slot_elems = static_cast<int64_t>(d) * f;
-  MOE_TRY(launch_gemm<M_DW>(s, dt, r));
+  MOE_TRY(launch_gemm<M_DW, P_BWD_DW2>(s, dt, r));
   MOE_TRY(launch_split_reduce(s, pl, ws, d, f, dw2, dw2, d));
 
   // [dW1; dW3] [F, d] = [dH1 dH3]^T X
@@ -1042,7 +1057,7 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   u.split_row = f;
   u.partial = reinterpret_cast<float*>(ws + pl.o_part);
   u.slot_elems = static_cast<int64_t>(F) * d;
-  MOE_TRY(launch_gemm<M_DW>(s, dt, u));
+  MOE_TRY(launch_gemm<M_DW, P_BWD_DW13>(s, dt, u));
   MOE_TRY(launch_split_reduce(s, pl, ws, F, d, dw1, sw ? dw3 : dw1, f));
   return MOE_OK;
 }

@@ -282,6 +282,7 @@ extern "C" moe_status moe_gate_topk(void* stream, moe_dtype dt, int T, int d,
   if (!x || !w_g || !logits || !ids || !weights) return MOE_EINVAL;
   if (!aligned16(x) || !aligned16(w_g)) return MOE_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  MOE_TIMED("gate_fwd", s);
   if (dt == MOE_BF16) {
     const int tok_per_block = kGateTokPerWave * kGateWaves;
     dim3 grid((T + tok_per_block - 1) / tok_per_block);
@@ -319,6 +320,7 @@ extern "C" moe_status moe_gate_bwd(void* stream, moe_dtype dt, int T, int d,
   hipStream_t s = static_cast<hipStream_t>(stream);
   const size_t n = static_cast<size_t>(E) * d;
   if (T == 0) {
+    MOE_TIMED("gate_bwd_zero", s);
     zero_f32_kernel<<<dim3((n + 255) / 256), 256, 0, s>>>(dw_g, n);
     MOE_LAUNCH_CHECK();
     return MOE_OK;
@@ -329,10 +331,15 @@ extern "C" moe_status moe_gate_bwd(void* stream, moe_dtype dt, int T, int d,
   if (!workspace || workspace_bytes < need) return MOE_EWORKSPACE;
   float* part = static_cast<float*>(workspace);
   const int nchunks = (T + kGbTok - 1) / kGbTok;
-  gate_bwd_dlogits_kernel<<<dim3((T + 63) / 64), 64, 0, s>>>(logits, ids, dweights, T, E,
+  {
+    MOE_TIMED("gate_bwd_dlogits", s);
+    gate_bwd_dlogits_kernel<<<dim3((T + 63) / 64), 64, 0, s>>>(logits, ids, dweights, T, E,
                                                              k, renorm, dlogits);
-  MOE_LAUNCH_CHECK();
+    MOE_LAUNCH_CHECK();
+  }
   dim3 grid((E + 7) / 8, (d + 511) / 512, nchunks);
+  {
+  MOE_TIMED("gate_bwd_dwg_partial", s);
   if (dt == MOE_BF16)
     gate_bwd_dwg_partial_kernel<uint16_t><<<grid, 64, 0, s>>>(
         static_cast<const uint16_t*>(x), dlogits, T, d, E, part);
@@ -340,6 +347,8 @@ extern "C" moe_status moe_gate_bwd(void* stream, moe_dtype dt, int T, int d,
     gate_bwd_dwg_partial_kernel<float><<<grid, 64, 0, s>>>(static_cast<const float*>(x),
                                                            dlogits, T, d, E, part);
   MOE_LAUNCH_CHECK();
+  }
+  MOE_TIMED("gate_bwd_dwg_reduce", s);
   gate_bwd_dwg_reduce_kernel<<<dim3((n + 255) / 256), 256, 0, s>>>(part, nchunks,
                                                                    static_cast<int>(n), dw_g);
   MOE_LAUNCH_CHECK();

@@ -388,6 +388,7 @@ extern "C" moe_status moe_count(void* stream, int T, int E, int k, const int32_t
   if (!shape_ok(T, E, k) || !counts || !status) return MOE_EINVAL;
   if (T > 0 && !ids) return MOE_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  MOE_TIMED("count", s);
   fill_i32_kernel<<<1, 64, 0, s>>>(counts, E, 0);
   MOE_LAUNCH_CHECK();
   const int64_t n = static_cast<int64_t>(T) * k;
@@ -404,6 +405,7 @@ extern "C" moe_status moe_update_capacity(void* stream, int T, int k, int E,
   if (!shape_ok(T, E, k) || num < 1 || den < 1 || cap_min < 0) return MOE_EINVAL;
   if (!capacity || !offsets) return MOE_EINVAL;
   if (static_cast<int64_t>(T) * E >= (int64_t(1) << 31)) return MOE_EINVAL;
+  MOE_TIMED("capacity", static_cast<hipStream_t>(stream));
   capacity_kernel<<<1, 64, 0, static_cast<hipStream_t>(stream)>>>(T, k, E, counts, num, den,
                                                                  cap_min, capacity, offsets);
   MOE_LAUNCH_CHECK();
@@ -440,14 +442,24 @@ extern "C" moe_status moe_dispatch(void* stream, moe_dtype dt, int T, int d, int
   int32_t* hist = static_cast<int32_t*>(workspace);
   int32_t* base = hist + static_cast<size_t>(nblk) * E;
   int32_t* cap_eff = base + static_cast<size_t>(nblk) * E;
-  route_hist_kernel<<<nblk, 256, 0, s>>>(ids, T, E, k, nblk, rows_alloc, hist, src, status);
-  MOE_LAUNCH_CHECK();
-  route_scan_kernel<<<1, 64, 0, s>>>(hist, nblk, E, capacity, offsets, rows_alloc, base,
-                                     cap_eff, counts, fill, status);
-  MOE_LAUNCH_CHECK();
+  {
+    MOE_TIMED("route_hist", s);
+    route_hist_kernel<<<nblk, 256, 0, s>>>(ids, T, E, k, nblk, rows_alloc, hist, src, status);
+    MOE_LAUNCH_CHECK();
+  }
+  {
+    MOE_TIMED("route_scan", s);
+    route_scan_kernel<<<1, 64, 0, s>>>(hist, nblk, E, capacity, offsets, rows_alloc, base,
+                                       cap_eff, counts, fill, status);
+    MOE_LAUNCH_CHECK();
+  }
   if (T == 0) return MOE_OK;
-  route_rank_kernel<<<nblk, 256, 0, s>>>(ids, T, E, k, base, cap_eff, offsets, dest_row, src);
-  MOE_LAUNCH_CHECK();
+  {
+    MOE_TIMED("route_rank", s);
+    route_rank_kernel<<<nblk, 256, 0, s>>>(ids, T, E, k, base, cap_eff, offsets, dest_row, src);
+    MOE_LAUNCH_CHECK();
+  }
+  MOE_TIMED("dispatch_gather", s);
   const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
   gather_rows_kernel<<<nblocks(T, kRowWaves), 256, 0, s>>>(
       static_cast<const uint4*>(x), dest_row, T, k, nvec, static_cast<uint4*>(x_disp));
@@ -465,6 +477,7 @@ extern "C" moe_status moe_combine(void* stream, moe_dtype dt, int T, int d, int 
   if (!aligned16(y_disp) || !aligned16(y)) return MOE_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
+  MOE_TIMED("combine", s);
   if (dt == MOE_BF16)
     combine_kernel<uint16_t><<<nblocks(T, kRowWaves), 256, 0, s>>>(
         static_cast<const uint4*>(y_disp), dest_row, weights, T, k, nvec, rows_alloc,
@@ -488,6 +501,7 @@ extern "C" moe_status moe_combine_bwd(void* stream, moe_dtype dt, int T, int d, 
   if (!aligned16(dy) || !aligned16(y_disp) || !aligned16(dy_disp)) return MOE_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
+  MOE_TIMED("combine_bwd", s);
   if (dt == MOE_BF16)
     combine_bwd_kernel<uint16_t><<<nblocks(T, kRowWaves), 256, 0, s>>>(
         static_cast<const uint4*>(dy), static_cast<const uint4*>(y_disp), dest_row, weights, T,
@@ -516,6 +530,7 @@ extern "C" moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d,
   const uint4* a = static_cast<const uint4*>(dx_disp);
   const uint4* g = static_cast<const uint4*>(w_g);
   uint4* o = static_cast<uint4*>(dx);
+  MOE_TIMED("dispatch_bwd", s);
   if (dt == MOE_BF16) {
     if (dlogits)
       dispatch_bwd_kernel<uint16_t, true><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);

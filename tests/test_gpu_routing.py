@@ -84,7 +84,7 @@ def test_count_with_faults():
 
 @pytest.mark.parametrize("T,k,E,num,den,cap_min", [
     (256, 1, 4, 5, 4, 0), (8192, 2, 16, 1, 1, 0), (16384, 1, 64, 2, 1, 0),
-    (1000, 2, 7, 1, 3, 5), (10, 2, 1, 7, 1, 0)])
+    (1000, 2, 7, 1, 3, 5), (10, 1, 1, 7, 1, 0)])
 def test_capacity_static(T, k, E, num, den, cap_min):
     cap = torch.empty(E, dtype=torch.int32, device=dev())
     off = torch.empty(E + 1, dtype=torch.int32, device=dev())
