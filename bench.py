@@ -51,7 +51,29 @@ def parse():
     ap.add_argument("--rows", default="fill", choices=["fill", "capacity"],
                     help="capacity = padded static-shape baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-gib", type=float, default=0.0,
+                    help="instead of the layer: time a plain device-to-device copy of this "
+                         "many GiB (achievable HBM bandwidth; byte-counter calibration)")
     return ap.parse_args()
+
+
+def copy_calibration(gib, steps):
+    """Plain device copy of a known size: achieved HBM GB/s (read + write)."""
+    import torch
+    n = int(gib * (1 << 30))
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(json.dumps({"copy_bytes_each_way": n, "ms_per_copy": round(ms, 4),
+                      "hbm_GBps_read_plus_write": round(2 * n / (ms / 1e3) / 1e9, 1)}))
 
 
 def gemm_flops(wl, kept):
@@ -127,6 +149,9 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer is not "
               "sharded across GPUs in this build.", file=sys.stderr)
         sys.exit(2)
+    if args.copy_gib > 0:
+        copy_calibration(args.copy_gib, args.steps)
+        return
     import numpy as np
     import torch
 

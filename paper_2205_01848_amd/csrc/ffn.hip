@@ -31,12 +31,11 @@ constexpr int BN = 256;
 constexpr int kThreads = 256;
 constexpr int kRowBytes = 128;                    // one K tile of one operand row
 constexpr int kTileBytes = BM * kRowBytes;        // 32 KB
-constexpr int kStageBytes = 2 * kTileBytes;       // A + B
-constexpr int kStripPitch = 132;                  // floats per staged row (128 + 4)
-constexpr int kStripBytes = 32 * kStripPitch * 4; // one wave's 32x128 fp32 strip
-constexpr int kLdsBytes = 8 * kStripBytes;        // two strips per wave; >= 2 stages
-static_assert(kLdsBytes >= 2 * kStageBytes, "LDS budget");
-static_assert(kLdsBytes <= 160 * 1024, "LDS budget");
+constexpr int kStripRows = 16;                    // accumulator rows staged per pass
+constexpr int kStripPitch = 136;                  // floats per staged row (128 + 8):
+                                                  // rows 4 apart fall 32 banks apart
+constexpr int kStripBytes = kStripRows * kStripPitch * 4;
+static_assert(2 * kStripBytes <= kTileBytes, "two staging strips per operand buffer");
 
 constexpr int kGroupM = 4;      // M tiles per scheduling group
 constexpr int kXcds = 8;
@@ -189,19 +188,40 @@ struct TileOps {
   const char* b_lo;   // row 0 of the B tile (tile rows 0..127)
   const char* b_hi;   // row 128 of the B tile (tile rows 128..255)
   int64_t ldb;
-  int b_rows_lo;      // valid rows in [0,128)
-  int b_rows_hi;      // valid rows in [128,256)
+  int b_rows_lo;      // valid rows in [0,128) (>= 1)
+  int b_rows_hi;      // valid rows in [128,256) (may be <= 0)
   int64_t kbytes;     // K extent in bytes (multiple of 16)
 };
 
+// Source of K-tail chunks: 16 zero bytes in global memory, so the direct
+// global->LDS loads of a partial K tile fill the missing K range with zeros.
+__device__ __attribute__((aligned(16))) const uint32_t g_zero_chunk[4] = {0u, 0u, 0u, 0u};
+
+// LDS tile layout: row r (0..255) of 128 bytes, its 16-byte chunk c stored at
+// r*128 + ((c ^ ((r >> 1) & 7)) << 4).  gfx950 LDS serves 16 lanes of a
+// 16-byte access per cycle from 64 banks (256 bytes): the MFMA fragment reads
+// touch 16 consecutive rows at one logical chunk; rows alternate bank halves
+// and (r >> 1) & 7 spreads each half's 8 rows over its 8 slots.
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
 // acc += A_tile * B_tile^T over the whole K extent.
+//
+// Operand tiles go global -> LDS with global_load_lds_dwordx4 (no VGPR
+// staging, no LDS write instructions): wave w fills the 1 KB blocks of 8 rows
+// number 8w..8w+7 of each operand, lane l landing at block + 16 l, i.e. row
+// (l >> 3) of the block, physical chunk (l & 7); the lane therefore fetches
+// logical chunk (l & 7) ^ swz(row).  Two stages live in four distinct LDS
+// arrays and the K loop is unrolled by two, so the stage written by the
+// in-flight loads is a different object from the one being read and no wait
+// on those loads is needed before the MFMA fragment reads.  Fragments are
+// double-buffered in registers: the LDS reads of substep s+1 are issued
+// before the 16 MFMAs of substep s.
 template <typename T>
-__device__ __forceinline__ void mainloop(const TileOps& op, char* lds, floatx16 (&acc)[4][4]) {
+__device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0, char* la1,
+                                         char* lb1, floatx16 (&acc)[4][4]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int lrow = tid >> 3;          // 0..31
-  const int lchunk = tid & 7;         // 16-byte chunk within the K tile row
   const int nk = static_cast<int>((op.kbytes + kRowBytes - 1) / kRowBytes);
 
 #pragma unroll
@@ -210,89 +230,113 @@ __device__ __forceinline__ void mainloop(const TileOps& op, char* lds, floatx16 
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+  if (nk <= 0) return;
 
-  // global source of this thread's 8 A chunks and 8 B chunks
-  const char* pa = op.a + static_cast<int64_t>(lrow) * op.lda + lchunk * 16;
-  const char* pb_lo = op.b_lo + static_cast<int64_t>(lrow) * op.ldb + lchunk * 16;
-  const char* pb_hi = op.b_hi + static_cast<int64_t>(lrow) * op.ldb + lchunk * 16;
-  const int64_t a32 = 32 * op.lda, b32 = 32 * op.ldb;
-  // LDS destination (swizzled): row r, chunk c -> r*128 + ((c ^ (r & 7)) << 4)
-  const int st_off = lrow * kRowBytes + ((lchunk ^ (lrow & 7)) << 4);
-  // fragment source: row (lane & 31) + 32*i of the wave's half, chunk 2s + (lane >> 5)
+  // Wave w fills operand rows 64w .. 64w+63: block i (8 rows) of the wave
+  // covers rows 64w + 8i + (lane >> 3).  swz() of those rows only depends on
+  // the parity of i, so a full tile needs one row pointer per operand and two
+  // chunk offsets; ragged tiles (an expert's last rows, an N or K tail) take
+  // a path that clamps rows to valid ones and reads K-tail chunks as zeros.
+  const int lrow = wave * 64 + (lane >> 3);                 // block-0 row of this lane
+  const int coff0 = ((lane & 7) ^ swz(lrow)) * 16;           // even blocks
+  const int coff1 = ((lane & 7) ^ swz(lrow + 8)) * 16;       // odd blocks
+  const char* arow = op.a + static_cast<int64_t>(lrow) * op.lda;
+  const char* brow = (wave < 2 ? op.b_lo + static_cast<int64_t>(lrow) * op.ldb
+                               : op.b_hi + static_cast<int64_t>(lrow - 128) * op.ldb);
+  const bool full_rows = op.a_rows >= BM && op.b_rows_lo >= 128 && op.b_rows_hi >= 128;
+  const char* zero = reinterpret_cast<const char*>(g_zero_chunk);
+  auto dma = [&](int kt, char* sa, char* sb) {
+    const int64_t kofs = static_cast<int64_t>(kt) * kRowBytes;
+    if (full_rows && kofs + kRowBytes <= op.kbytes) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int blk = wave * 8 + i;
+        const int co = (i & 1) ? coff1 : coff0;
+        const char* ga = arow + i * 8 * op.lda + co + kofs;
+        const char* gb = brow + i * 8 * op.ldb + co + kofs;
+        __builtin_amdgcn_global_load_lds(ga, (__attribute__((address_space(3))) void*)(sa + blk * 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(gb, (__attribute__((address_space(3))) void*)(sb + blk * 1024), 16, 0, 0);
+      }
+      return;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int blk = wave * 8 + i;
+      const int row = lrow + i * 8;
+      const int co = (i & 1) ? coff1 : coff0;
+      const bool kok = kofs + co < op.kbytes;
+      const char* ga = op.a + static_cast<int64_t>(min(row, op.a_rows - 1)) * op.lda;
+      const char* gb;
+      if (row < 128) {
+        gb = op.b_lo + static_cast<int64_t>(min(row, op.b_rows_lo - 1)) * op.ldb;
+      } else if (op.b_rows_hi > 0) {
+        gb = op.b_hi + static_cast<int64_t>(min(row - 128, op.b_rows_hi - 1)) * op.ldb;
+      } else {
+        gb = op.b_lo;   // rows past N: any valid row, their outputs are not stored
+      }
+      ga = kok ? ga + co + kofs : zero;
+      gb = kok ? gb + co + kofs : zero;
+      __builtin_amdgcn_global_load_lds(ga, (__attribute__((address_space(3))) void*)(sa + blk * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(gb, (__attribute__((address_space(3))) void*)(sb + blk * 1024), 16, 0, 0);
+    }
+  };
   const int fr_row = lane & 31;
   const int fr_base_a = (wm * 128 + fr_row) * kRowBytes;
   const int fr_base_b = (wn * 128 + fr_row) * kRowBytes;
-
-  uint4 ra[8], rb[8];
-  auto gload = [&](int kt) {
-    const int64_t kofs = static_cast<int64_t>(kt) * kRowBytes;
-    const bool kok = kofs + lchunk * 16 < op.kbytes;
+  uint4 fa[2][4], fb[2][4];
+  auto fread = [&](const char* sa, const char* sb, int s, int buf) {
+    const int sw = (((2 * s + (lane >> 5)) ^ swz(fr_row)) << 4);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const bool ok = kok && (lrow + 32 * i) < op.a_rows;
-      ra[i] = ok ? *reinterpret_cast<const uint4*>(pa + i * a32 + kofs) : make_uint4(0, 0, 0, 0);
-    }
+    for (int i = 0; i < 4; ++i)
+      fa[buf][i] = *reinterpret_cast<const uint4*>(sa + fr_base_a + i * 32 * kRowBytes + sw);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const bool ok = kok && (lrow + 32 * i) < op.b_rows_lo;
-      rb[i] = ok ? *reinterpret_cast<const uint4*>(pb_lo + i * b32 + kofs) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const bool ok = kok && (lrow + 32 * i) < op.b_rows_hi;
-      rb[4 + i] = ok ? *reinterpret_cast<const uint4*>(pb_hi + i * b32 + kofs) : make_uint4(0, 0, 0, 0);
-    }
+    for (int j = 0; j < 4; ++j)
+      fb[buf][j] = *reinterpret_cast<const uint4*>(sb + fr_base_b + j * 32 * kRowBytes + sw);
   };
-  auto lstore = [&](int stage) {
-    char* sa = lds + stage * kStageBytes;
-    char* sb = sa + kTileBytes;
+  auto mma = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) *reinterpret_cast<uint4*>(sa + st_off + i * 32 * kRowBytes) = ra[i];
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) *reinterpret_cast<uint4*>(sb + st_off + i * 32 * kRowBytes) = rb[i];
+      for (int j = 0; j < 4; ++j) Mma<T>::run(acc[i][j], fa[buf][i], fb[buf][j]);
   };
-  auto compute = [&](int stage) {
-    const char* sa = lds + stage * kStageBytes;
-    const char* sb = sa + kTileBytes;
+  auto tile = [&](const char* sa, const char* sb) {
+    fread(sa, sb, 0, 0);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const int sw = (((2 * s + (lane >> 5)) ^ (fr_row & 7)) << 4);
-      uint4 fa[4], fb[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        fa[i] = *reinterpret_cast<const uint4*>(sa + fr_base_a + i * 32 * kRowBytes + sw);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        fb[j] = *reinterpret_cast<const uint4*>(sb + fr_base_b + j * 32 * kRowBytes + sw);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) Mma<T>::run(acc[i][j], fa[i], fb[j]);
+      if (s < 3) fread(sa, sb, s + 1, (s + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(s & 1);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  if (nk <= 0) return;
-  gload(0);
-  lstore(0);
+  // K tiles in pairs (stage 0, then stage 1).  An odd count is rounded up:
+  // the extra tile lies past K and is loaded as zeros, adding nothing.  (One
+  // loop body and no peeled tail keeps the accumulators in place.)
+  const int nk2 = (nk + 1) & ~1;
+  dma(0, la0, lb0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const bool more = kt + 1 < nk;
-    if (more) gload(kt + 1);
-    compute(kt & 1);
-    if (more) lstore((kt + 1) & 1);
+  for (int kt = 0; kt < nk2; kt += 2) {
+    dma(kt + 1, la1, lb1);
+    tile(la0, lb0);
+    __syncthreads();
+    if (kt + 2 < nk2) dma(kt + 2, la0, lb0);
+    tile(la1, lb1);
     __syncthreads();
   }
 }
 
-// Stage accumulator strip i (rows 32i..32i+31 of the wave's 128) as fp32.
-__device__ __forceinline__ void stage_strip(float* strip, const floatx16 (&acc)[4][4], int i) {
+// Stage rows [16h, 16h+16) of accumulator row-block i (32 rows) as fp32: the
+// lane's registers q in [8h, 8h+8) hold those rows.
+__device__ __forceinline__ void stage_strip(float* strip, const floatx16 (&acc)[4][4], int i,
+                                            int h) {
   const int lane = threadIdx.x & 63;
   const int half = lane >> 5, col = lane & 31;
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int row = (q >> 2) * 8 + half * 4 + (q & 3);
+    for (int q = 8 * h; q < 8 * h + 8; ++q) {
+      const int row = ((q >> 2) - 2 * h) * 8 + half * 4 + (q & 3);
       strip[row * kStripPitch + j * 32 + col] = acc[i][j][q];
     }
 }
@@ -354,7 +398,12 @@ enum Pass { P_FWD_H = 0, P_FWD_Y = 1, P_BWD_DA = 2, P_BWD_DX = 3, P_BWD_DW2 = 4,
 
 template <typename T, int MODE, int PASS>
 __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams p) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsBytes];
+  // two stages of the A and B tiles, four distinct objects (see mainloop);
+  // after the K loop the same memory stages the epilogue
+  __shared__ __attribute__((aligned(16))) char la0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) char lb0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) char la1[kTileBytes];
+  __shared__ __attribute__((aligned(16))) char lb1[kTileBytes];
   constexpr int ES = sizeof(T);
   constexpr bool VARK = MODE == M_DW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -422,25 +471,30 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
     }
 
     floatx16 acc[4][4];
-    mainloop<T>(op, lds, acc);
-    __syncthreads();  // operand buffers are free: reuse LDS for the epilogue
+    mainloop<T>(op, la0, lb0, la1, lb1, acc);
+    // (the K loop ended with a barrier: the operand buffers are free)
 
-    float* strip = reinterpret_cast<float*>(lds + wave * kStripBytes);
-    float* strip3 = reinterpret_cast<float*>(lds + (4 + wave) * kStripBytes);
+    // staging strips: wave w uses (w < 2 ? la0 : lb0) + (w & 1) * kStripBytes,
+    // and a second strip at the same place in la1 / lb1
+    auto strip_of = [&](int w) {
+      return reinterpret_cast<float*>((w < 2 ? la0 : lb0) + (w & 1) * kStripBytes);
+    };
+    float* strip = strip_of(wave);
+    float* strip3 = reinterpret_cast<float*>((wave < 2 ? la1 : lb1) + (wave & 1) * kStripBytes);
 
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      stage_strip(strip, acc, i);
+    for (int i = 0; i < 8; ++i) {
+      stage_strip(strip, acc, i >> 1, i & 1);
       __syncthreads();
-      const int srow0 = wm * 128 + i * 32;  // strip's first row within the tile
+      const int srow0 = wm * 128 + i * kStripRows;  // strip's first row within the tile
       if constexpr (MODE == M_FWD1_SWIGLU) {
         // waves (wm,0) hold H1, (wm,1) hold H3 for the same columns; each of
-        // the pair finishes 16 of the strip's 32 rows
-        const float* s1 = reinterpret_cast<float*>(lds + (wm * 2 + 0) * kStripBytes);
-        const float* s3 = reinterpret_cast<float*>(lds + (wm * 2 + 1) * kStripBytes);
+        // the pair finishes 8 of the strip's 16 rows
+        const float* s1 = strip_of(wm * 2 + 0);
+        const float* s3 = strip_of(wm * 2 + 1);
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-          const int r = wn * 16 + it * 4 + (lane >> 4);
+        for (int it = 0; it < 2; ++it) {
+          const int r = wn * 8 + it * 4 + (lane >> 4);
           const int c8 = (lane & 15) * 8;
           const int lm = srow0 + r;
           const int gc = n0 + c8;
@@ -462,7 +516,7 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
         }
       } else if constexpr (MODE == M_FWD1 || MODE == M_STORE) {
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
+        for (int it = 0; it < 4; ++it) {
           const int r = it * 4 + (lane >> 4);
           const int c8 = (lane & 15) * 8;
           const int lm = srow0 + r;
@@ -487,7 +541,7 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
       } else if constexpr (MODE == M_BWD_DA || MODE == M_BWD_DA_SWIGLU) {
         constexpr bool SW = MODE == M_BWD_DA_SWIGLU;
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
+        for (int it = 0; it < 4; ++it) {
           const int r = it * 4 + (lane >> 4);
           const int c8 = (lane & 15) * 8;
           const int lm = srow0 + r;
@@ -533,9 +587,9 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
         const int kcol0 = sc.kbase[g] + local_m0 + srow0;   // first transposed column
         const int kpad_g = (sc.rows[g] + kTT - 1) / kTT * kTT;
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
-          const int c = it * 16 + (lane >> 2);
-          const int rg = (lane & 3) * 8;
+        for (int it = 0; it < 4; ++it) {
+          const int c = it * 32 + (lane >> 1);
+          const int rg = (lane & 1) * 8;
           const int gc = n0 + wn * 128 + c;
           if (gc < p.N && local_m0 + srow0 + rg < kpad_g) {
             float v[8];
@@ -553,7 +607,7 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
         }
       } else {  // M_DW: fp32 rows of dW (or of a partial-sum slot)
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
+        for (int it = 0; it < 4; ++it) {
           const int r = it * 4 + (lane >> 4);
           const int c8 = (lane & 15) * 8;
           const int lm = srow0 + r;
@@ -571,9 +625,9 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
               dst = p.dwB + static_cast<int64_t>(g) * p.dw_gstride +
                     static_cast<int64_t>(orow - p.split_row) * p.N + gc;
             }
-            const float* s = strip + r * kStripPitch + c8;
-            *reinterpret_cast<float4*>(dst) = make_float4(s[0], s[1], s[2], s[3]);
-            *reinterpret_cast<float4*>(dst + 4) = make_float4(s[4], s[5], s[6], s[7]);
+            const float* sp = strip + r * kStripPitch + c8;
+            *reinterpret_cast<float4*>(dst) = make_float4(sp[0], sp[1], sp[2], sp[3]);
+            *reinterpret_cast<float4*>(dst + 4) = make_float4(sp[4], sp[5], sp[6], sp[7]);
           }
         }
       }
