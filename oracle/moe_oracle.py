@@ -49,7 +49,8 @@ __all__ = [
     "validate_assignments", "count_assignments",
     "capacity_static", "capacity_dynamic", "exclusive_offsets",
     "assign_slots", "dispatch_rows",
-    "act_fwd", "act_grad", "ffn_rows_fwd", "ffn_rows_bwd",
+    "act_fwd", "act_grad", "ffn_rows_fwd", "ffn_rows_bwd", "ffn_dw_slices",
+    "topk_alternatives",
     "combine", "combine_bwd", "gate_bwd", "dispatch_bwd",
     "route", "layer_forward", "layer_backward",
 ]
@@ -388,6 +389,58 @@ def ffn_rows_bwd(X: np.ndarray, e_of_row: np.ndarray, H: np.ndarray,
         dW1[e] = _f32(g1.T @ Xe)
         dW2[e] = _f32(dYe.T @ a)
     return dict(dX=dX, dH=dH, dH3=dH3, dW1=dW1, dW2=dW2, dW3=dW3)
+
+
+def ffn_dw_slices(X: np.ndarray, dY: np.ndarray, w1_e: np.ndarray,
+                  w3_e: Optional[np.ndarray], w2_e: np.ndarray, act: str, dtype: str,
+                  cols: np.ndarray) -> Dict[str, np.ndarray]:
+    """Slices of one expert's weight gradients, by the same definitions as
+    ffn_rows_bwd restricted to hidden units `cols` (for checks at sizes where
+    the full gradient is too costly): dW2[:, cols] (d x n), dW1[cols, :] and
+    dW3[cols, :] (n x d).  X, dY are all of the expert's rows."""
+    J = np.asarray(cols, dtype=np.int64)
+    h = round_to(X @ w1_e[J].T, dtype)
+    dA = dY @ w2_e[:, J]
+    if act == "swiglu":
+        h3 = round_to(X @ w3_e[J].T, dtype)
+        a = round_to(act_fwd(h, "silu") * h3, dtype)
+        g1 = round_to(dA * h3 * act_grad(h, "silu"), dtype)
+        g3 = round_to(dA * act_fwd(h, "silu"), dtype)
+    else:
+        a = round_to(act_fwd(h, act), dtype)
+        g1 = round_to(dA * act_grad(h, act), dtype)
+        g3 = None
+    out = dict(dW2=_f32(dY.T @ a), dW1=_f32(g1.T @ X))
+    out["dW3"] = None if g3 is None else _f32(g3.T @ X)
+    return out
+
+
+def topk_alternatives(logits: np.ndarray, k: int, tol: float) -> list:
+    """Valid top-k lists of one token when logits closer than `tol` are taken
+    as tied (their order is not decided by the arithmetic): start from the
+    strict order (ties to the lower index) and apply every adjacent swap of
+    near-tied logits among the positions that can reach the first k picks."""
+    l = np.asarray(logits, dtype=np.float64)
+    order = list(np.argsort(-l, kind="stable"))
+    # positions that can reach the first k picks: the first k, extended
+    # through any chain of near ties across the k-th / (k+1)-th boundary
+    r = k
+    while r < len(order) and abs(l[order[r - 1]] - l[order[r]]) <= tol:
+        r += 1
+    seen = {tuple(order)}
+    frontier = [order]
+    while frontier:
+        nxt = []
+        for o in frontier:
+            for p in range(min(r, len(o)) - 1):
+                if abs(l[o[p]] - l[o[p + 1]]) <= tol:
+                    q = list(o)
+                    q[p], q[p + 1] = q[p + 1], q[p]
+                    if tuple(q) not in seen:
+                        seen.add(tuple(q))
+                        nxt.append(q)
+        frontier = nxt
+    return sorted({tuple(o[:k]) for o in seen})
 
 
 # ----------------------------------------------------------------------------

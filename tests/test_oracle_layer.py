@@ -250,3 +250,39 @@ def test_dropped_tokens_do_not_reach_weight_gradients():
     np.testing.assert_array_equal(b1["dW1"], b2["dW1"])
     np.testing.assert_array_equal(b1["dW2"], b2["dW2"])
     assert (b2["dx"][dropped_only] == 0).all()
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_dw_slices_match_full_backward(act):
+    """The column-slice form of the weight gradients equals the full
+    backward's gradients on the same columns (bf16 rounding points)."""
+    rng = np.random.default_rng(70)
+    R, d, f = 57, 24, 40
+    X = O.round_bf16(rng.standard_normal((R, d)))
+    dY = O.round_bf16(rng.standard_normal((R, d)))
+    w1 = O.round_bf16(rng.standard_normal((1, f, d)) * 0.2)
+    w3 = O.round_bf16(rng.standard_normal((1, f, d)) * 0.2) if act == "swiglu" else None
+    w2 = O.round_bf16(rng.standard_normal((1, d, f)) * 0.2)
+    e_of = np.zeros(R, dtype=np.int64)
+    fw = O.ffn_rows_fwd(X, e_of, w1, w3, w2, act, "bf16")
+    bw = O.ffn_rows_bwd(X, e_of, fw["H"], fw["H3"], dY, w1, w3, w2, act, "bf16", 1)
+    cols = np.array([0, 7, 39, 12])
+    sl = O.ffn_dw_slices(X, dY, w1[0], None if w3 is None else w3[0], w2[0], act, "bf16", cols)
+    np.testing.assert_array_equal(sl["dW2"], bw["dW2"][0][:, cols])
+    np.testing.assert_array_equal(sl["dW1"], bw["dW1"][0][cols])
+    if act == "swiglu":
+        np.testing.assert_array_equal(sl["dW3"], bw["dW3"][0][cols])
+
+
+def test_topk_alternatives():
+    l = np.array([1.0, 3.0, 3.0 + 1e-9, 0.5])
+    alts = O.topk_alternatives(l, 2, 1e-6)
+    assert (2, 1) in alts and (1, 2) in alts and len(alts) == 2
+    alts = O.topk_alternatives(np.array([2.0, 1.0, 1.0 + 1e-9, 1.0 - 1e-9]), 2, 1e-6)
+    assert set(alts) == {(0, 2), (0, 1), (0, 3)}
+    assert O.topk_alternatives(np.array([0.0, 1.0, 2.0]), 2, 1e-6) == [(2, 1)]
+    # strict order equals topk() when nothing is near-tied
+    l = np.random.default_rng(3).standard_normal((50, 6)).astype(np.float32)
+    ids = O.topk(l, 3)
+    for t in range(50):
+        assert O.topk_alternatives(l[t], 3, 0.0) == [tuple(ids[t])]
