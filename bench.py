@@ -104,6 +104,21 @@ def hbm_bytes(wl, kept, active):
     return b
 
 
+def profiled_traffic(workload, kernel):
+    """Calibrated HBM bytes per launch of `kernel` from profiles/traffic_<workload>.json,
+    or None when the summary is missing or the kernels changed since."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    from paper_2205_01848_amd.rocprof_summary import source_hash
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_hash") != source_hash() or kernel not in t.get("kernels", {}):
+        return None
+    k = t["kernels"][kernel]
+    return int(k["read_bytes"] + k["write_bytes"])
+
+
 def cpu_baseline(wl, I, cap_rule, ntok):
     """The oracle as it stands, on the first `ntok` tokens of the batch (the
     same per-token work: gate, capacity on the sample's own counts,
@@ -243,12 +258,14 @@ def main():
         avg_s = ms / n / 1e3
         ach = fl_alg[dom] / avg_s / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1), "peak": peak,
-                "unit": "TFLOP/s", "frac": round(ach / peak, 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                "traffic": profiled_traffic(args.workload, dom)}
     elif dom in by:
         n, ms = kern[dom]
         ach = by[dom] / (ms / n / 1e3) / 1e9
         roof = {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                "traffic": profiled_traffic(args.workload, dom)}
     gemm_ms = sum(kern[k][1] for k in kern if k in fl)
     gemm_fl = sum(fl_alg[k] * kern[k][0] for k in kern if k in fl)
 

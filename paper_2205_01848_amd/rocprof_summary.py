@@ -1,0 +1,133 @@
+"""Summarise rocprofv3 output of a bench.py run into profiles/.
+
+    python -m paper_2205_01848_amd.rocprof_summary --workload c5 \\
+        --stats <dir>/c5_kernel_stats.csv \\
+        --fetch <dir>/fetch_counter_collection.csv --write <dir>/write_counter_collection.csv \\
+        --copy-fetch <dir>/copyf_counter_collection.csv \\
+        --copy-write <dir>/copyw_counter_collection.csv --copy-bytes 1073741824 \\
+        --command "..." [--command "..."] --out profiles/<name>.md --json profiles/<name>.json
+
+Byte counters are calibrated with a plain device copy of known size:
+factor = copy bytes / (counter KiB * 1024) for FETCH_SIZE and WRITE_SIZE
+separately, and every kernel's per-dispatch KiB is scaled by its factor.
+The JSON keeps the calibrated bytes per dispatch and a hash of the HIP
+sources, so bench.py reports them only while the kernels are unchanged.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import hashlib
+import json
+import os
+import re
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+PASS_NAMES = ["gemm_fwd_h", "gemm_fwd_y", "gemm_bwd_da", "gemm_bwd_dx", "gemm_bwd_dw2",
+              "gemm_bwd_dw13"]
+
+
+def source_hash() -> str:
+    """sha256 over the library's HIP sources and headers (sorted by name)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(HERE, "csrc")
+    for fn in sorted(os.listdir(csrc)):
+        if fn.endswith((".hip", ".hpp")):
+            h.update(fn.encode())
+            with open(os.path.join(csrc, fn), "rb") as f:
+                h.update(f.read())
+    with open(os.path.join(HERE, "..", "include", "moe.h"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def short_name(name: str) -> str:
+    m = re.search(r"ffn_gemm_kernel<([^,]+), (\d+), (\d+)>", name)
+    if m:
+        return PASS_NAMES[int(m.group(3))] + ("" if "short" in m.group(1) else "_f32")
+    m = re.search(r"moe::(?:\(anonymous namespace\)::)?(\w+)(<[^(]*>)?", name)
+    if m:
+        targs = (m.group(2) or "").replace("unsigned short", "bf16").replace("float", "f32")
+        return m.group(1) + targs.replace(" ", "")
+    return re.sub(r"\(.*", "", name)[:60]
+
+
+def per_dispatch(path, counter):
+    """{short kernel name: mean counter value per dispatch}."""
+    acc = collections.defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter:
+                acc[short_name(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def copy_factor(path, counter, nbytes):
+    vals = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter and "copyBuffer" in r["Kernel_Name"]:
+                vals.append(float(r["Counter_Value"]))
+    kib = max(vals)
+    return nbytes / (kib * 1024.0), kib
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--stats", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--copy-fetch")
+    ap.add_argument("--copy-write")
+    ap.add_argument("--copy-bytes", type=float, default=float(1 << 30))
+    ap.add_argument("--command", action="append", default=[])
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--json")
+    a = ap.parse_args()
+
+    rows = []
+    with open(a.stats) as f:
+        for r in csv.DictReader(f):
+            rows.append((short_name(r["Name"]), int(r["Calls"]), float(r["AverageNs"]),
+                         float(r["TotalDurationNs"]), float(r["Percentage"])))
+    rows.sort(key=lambda r: -r[3])
+    lines = [f"# rocprofv3 summary: workload {a.workload}", "",
+             "Commands (run from /tmp with TMPDIR=/tmp; R = repository root):", ""]
+    lines += [f"    {c}" for c in a.command]
+    lines += ["", "## Kernel trace (--kernel-trace --stats)", "",
+              "| kernel | calls | avg ms | total ms | % |", "|---|---|---|---|---|"]
+    for n, c, avg, tot, pct in rows[:24]:
+        lines.append(f"| {n} | {c} | {avg / 1e6:.4f} | {tot / 1e6:.2f} | {pct:.2f} |")
+    out = {"workload": a.workload, "source_hash": source_hash(), "kernels": {}}
+    if a.fetch and a.write and a.copy_fetch and a.copy_write:
+        ff, fk = copy_factor(a.copy_fetch, "FETCH_SIZE", a.copy_bytes)
+        wf, wk = copy_factor(a.copy_write, "WRITE_SIZE", a.copy_bytes)
+        fetch = per_dispatch(a.fetch, "FETCH_SIZE")
+        write = per_dispatch(a.write, "WRITE_SIZE")
+        lines += ["", "## HBM traffic (--pmc FETCH_SIZE, then --pmc WRITE_SIZE; KiB per dispatch)",
+                  "",
+                  f"Calibration: a plain {a.copy_bytes / 2**30:.2f} GiB device copy reads "
+                  f"FETCH_SIZE = {fk:.0f} KiB and WRITE_SIZE = {wk:.0f} KiB, so FETCH_SIZE is "
+                  f"scaled by {ff:.3f} and WRITE_SIZE by {wf:.3f}.", "",
+                  "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | calibrated read GB | "
+                  "calibrated write GB |", "|---|---|---|---|---|"]
+        for n in sorted(set(fetch) & set(write), key=lambda n: -(fetch[n] + write[n])):
+            rb = fetch[n] * 1024 * ff
+            wb = write[n] * 1024 * wf
+            out["kernels"][n] = {"read_bytes": rb, "write_bytes": wb}
+            if rb + wb > 1e6:
+                lines.append(f"| {n} | {fetch[n]:.0f} | {write[n]:.0f} | {rb / 1e9:.3f} | "
+                             f"{wb / 1e9:.3f} |")
+        out["calibration"] = {"fetch_factor": ff, "write_factor": wf}
+    lines += ["", f"Kernel sources hash: {out['source_hash']}", ""]
+    with open(a.out, "w") as f:
+        f.write("\n".join(lines))
+    if a.json:
+        with open(a.json, "w") as f:
+            json.dump(out, f, indent=1)
+
+
+if __name__ == "__main__":
+    main()
