@@ -77,7 +77,8 @@ def copy_calibration(gib, steps):
 
 
 def gemm_flops(wl, kept):
-    """Algorithmic MFMA flops per GEMM pass over `kept` rows."""
+    """Algorithmic MFMA flops per GEMM pass over `kept` rows: 2 flops per multiply-add
+    of each rows x d x f product the pass computes (gated FFN: two for H1 and H3)."""
     unit = 2 * kept * wl.d * wl.f
     g = 2 if wl.act == "swiglu" else 1
     fl = {"gemm_fwd_h": g * unit, "gemm_fwd_y": unit}

@@ -167,3 +167,48 @@ def test_dispatch_is_exact_copy():
             if r >= 0:
                 assert (xd[r] == x[t]).all()
     assert np.isnan(xd[s["src"] < 0]).all()
+
+
+def test_hand_worked_example():
+    """A six-token, three-expert, top-2 batch worked out by hand from Eq. 4 and
+    the Section 3.1 rule (first entries of each expert tensor kept; priority:
+    first choices in token order, then second choices).
+
+    ids: t0 (0,1) t1 (0,2) t2 (1,0) t3 (0,1) t4 (2,0) t5 (0,2)
+    counts: e0 = 6, e1 = 3, e2 = 3.
+    Static alpha = 1: C = ceil(6*2/3) = 4 for every expert, offsets 0,4,8,12.
+      first choices: t0->e0 pos 0, t1->e0 1, t2->e1 0, t3->e0 2, t4->e2 0, t5->e0 3
+      second:        t0->e1 1, t1->e2 1, t2->e0 4 (drop), t3->e1 2, t4->e0 5 (drop),
+                     t5->e2 2
+    Dynamic 11/10: C = ceil(6.6), ceil(3.3), ceil(3.3) = 7, 4, 4, clamped to
+    T = 6 -> 6, 4, 4; offsets 0,6,10,14; nothing dropped.
+    Combine with Y_disp[r] = r + 1 (d = 1) under the static capacities:
+      y0 = .75*1 + .25*6 = 2.25   y1 = .5*2 + .5*10 = 6   y2 = .6*5 = 3
+      y3 = 1*3 + 0*7 = 3          y4 = .3*9 = 2.7         y5 = .2*4 + .8*11 = 9.6
+    """
+    ids = np.array([[0, 1], [0, 2], [1, 0], [0, 1], [2, 0], [0, 2]], dtype=np.int32)
+    counts = O.count_assignments(ids, 3)
+    assert list(counts) == [6, 3, 3]
+
+    cap = O.capacity_static(6, 2, 3, 1, 1)
+    assert list(cap) == [4, 4, 4]
+    off = O.exclusive_offsets(cap)
+    assert list(off) == [0, 4, 8, 12]
+    s = O.assign_slots(ids, 3, cap, off, 12)
+    assert s["dest_row"].tolist() == [[0, 5], [1, 9], [4, -1], [2, 6], [8, -1], [3, 10]]
+    assert list(s["fill"]) == [4, 3, 3]
+    assert list(s["src"]) == [0, 2, 6, 10, 4, 1, 7, -1, 8, 3, 11, -1]
+
+    w = np.array([[.75, .25], [.5, .5], [.6, .4], [1., 0.], [.3, .7], [.2, .8]])
+    Y = (np.arange(12, dtype=np.float64) + 1)[:, None]
+    y = O.combine(Y, s["dest_row"], w, "f32")
+    np.testing.assert_allclose(y[:, 0], [2.25, 6, 3, 3, 2.7, 9.6], rtol=1e-15)
+
+    capd = O.capacity_dynamic(counts, 6, 11, 10)
+    assert list(capd) == [6, 4, 4]
+    offd = O.exclusive_offsets(capd)
+    assert list(offd) == [0, 6, 10, 14]
+    sd = O.assign_slots(ids, 3, capd, offd, 14)
+    assert sd["dest_row"].tolist() == [[0, 7], [1, 11], [6, 4], [2, 8], [10, 5], [3, 12]]
+    assert list(sd["fill"]) == [6, 3, 3]
+    assert list(sd["src"]) == [0, 2, 6, 10, 5, 9, 4, 1, 7, -1, 8, 3, 11, -1]
