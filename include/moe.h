@@ -30,6 +30,9 @@
  *   linear map y = x W^T: w_g [E,d], w1 [E,f,d], w3 [E,f,d], w2 [E,d,f].
  * - Limits: 1 <= E <= 64, 1 <= k <= min(E, 8), T >= 0 (T = 0 is a valid
  *   empty batch), d, f >= 1 and multiples of 8, T*k and rows_alloc < 2^31.
+ *   The expert FFN calls further need (rows_alloc + 64 E + 63), d and 2 f
+ *   times the element size to stay below 2^23 bytes (e.g. rows_alloc up
+ *   to 4,000,000 in bf16, 2,000,000 in fp32); larger requests are EINVAL.
  * - Every output is deterministic run to run (no floating-point atomics).
  */
 #ifndef MOE_H_

@@ -3,10 +3,11 @@
 //
 // Every product is one persistent grouped GEMM kernel in "NT" form,
 //     C[m, n] = sum_k A[m, k] * B[n, k]     (both operands K-contiguous),
-// 256x256 output tiles, K tiles of 128 bytes, 4 wavefronts of 128x128 each
-// on v_mfma_f32_32x32x16_bf16 (fp32 layers: v_mfma_f32_32x32x2f32), operand
-// tiles double-buffered in LDS with an XOR swizzle so both the 16-byte
-// stores and the MFMA fragment reads are bank-conflict free.
+// 256x256 output tiles, K tiles of 128 bytes, 8 wavefronts of 128x64 each
+// on v_mfma_f32_32x32x16_bf16 (fp32 layers: v_mfma_f32_32x32x2f32) in two
+// ping-pong teams (one team's MFMAs overlap the other's LDS reads), operand
+// tiles loaded HBM -> LDS by buffer loads, double-buffered, with an XOR
+// swizzle that keeps the MFMA fragment reads bank-conflict free.
 //  * var-M products (forward H, Y; backward dA, dX): the M dimension of
 //    expert e is its row count, read on the device; tiles are listed by a
 //    one-workgroup schedule kernel, so no host synchronisation is needed.
@@ -17,8 +18,8 @@
 // contiguous run of tiles arranged as 4 M-tiles x 8 N-tiles, so tiles that
 // share operand panels share that XCD's L2.
 // Epilogues (activation, SwiGLU, activation backward, transposed stores) run
-// on the fp32 accumulators staged through LDS, 32 rows at a time, and write
-// 16-byte vectors.
+// per wavefront on its fp32 accumulators, staged 16 rows at a time through a
+// private LDS strip, and write 16-byte vectors.
 
 #include "common.hpp"
 #include "validate.hpp"
@@ -28,19 +29,21 @@ namespace {
 
 constexpr int BM = 256;
 constexpr int BN = 256;
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;                     // 8 wavefronts, two per SIMD
 constexpr int kRowBytes = 128;                    // one K tile of one operand row
 constexpr int kTileBytes = BM * kRowBytes;        // 32 KB
 constexpr int kStripRows = 16;                    // accumulator rows staged per pass
-constexpr int kStripPitch = 136;                  // floats per staged row (128 + 8):
+constexpr int kStripPitch = 72;                   // floats per staged row (64 + 8):
                                                   // rows 4 apart fall 32 banks apart
 constexpr int kStripBytes = kStripRows * kStripPitch * 4;
-static_assert(2 * kStripBytes <= kTileBytes, "two staging strips per operand buffer");
+constexpr int kStripsPerArray = kTileBytes / kStripBytes;
+static_assert(3 * kStripsPerArray >= 16, "two staging strips per wave in three operand buffers");
 
 constexpr int kGroupM = 4;      // M tiles per scheduling group
 constexpr int kXcds = 8;
 constexpr int kSplitFloor = 512;  // smallest K chunk of a split dW product
 constexpr int kTT = 64;           // transpose tile
+constexpr int64_t kMaxOperandRowBytes = (int64_t(1) << 23) - 64;  // 256 rows < 2^31 bytes
 
 enum Act { ACT_RELU = 0, ACT_GELU = 1, ACT_SWIGLU = 2 };
 
@@ -180,22 +183,18 @@ template <> struct Mma<float> {
   }
 };
 
-// One tile's operand description (byte pointers, byte strides).
+// One tile's operand description (byte pointers, byte strides).  Rows of a
+// tile at or past a_rows / b_rows, and K bytes at or past kbytes, read as 0.
 struct TileOps {
-  const char* a;      // row 0 of the A tile, k = 0
+  const char* a;      // A tile: row 0, k = 0
   int64_t lda;        // bytes between A rows
-  int a_rows;         // valid A rows (>= 1)
-  const char* b_lo;   // row 0 of the B tile (tile rows 0..127)
-  const char* b_hi;   // row 128 of the B tile (tile rows 128..255)
+  int a_rows;         // valid A rows
+  const char* b;      // B tile: row 0, k = 0
+  const char* b3;     // gated forward: the W3 rows (b holds W1), else null
   int64_t ldb;
-  int b_rows_lo;      // valid rows in [0,128) (>= 1)
-  int b_rows_hi;      // valid rows in [128,256) (may be <= 0)
-  int64_t kbytes;     // K extent in bytes (multiple of 16)
+  int b_rows;         // valid B rows (gated forward: valid hidden units)
+  int kbytes;         // K extent in bytes (multiple of 16)
 };
-
-// Source of K-tail chunks: 16 zero bytes in global memory, so the direct
-// global->LDS loads of a partial K tile fill the missing K range with zeros.
-__device__ __attribute__((aligned(16))) const uint32_t g_zero_chunk[4] = {0u, 0u, 0u, 0u};
 
 // LDS tile layout: row r (0..255) of 128 bytes, its 16-byte chunk c stored at
 // r*128 + ((c ^ ((r >> 1) & 7)) << 4).  gfx950 LDS serves 16 lanes of a
@@ -204,136 +203,162 @@ __device__ __attribute__((aligned(16))) const uint32_t g_zero_chunk[4] = {0u, 0u
 // and (r >> 1) & 7 spreads each half's 8 rows over its 8 slots.
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
-// acc += A_tile * B_tile^T over the whole K extent.
-//
-// Operand tiles go global -> LDS with global_load_lds_dwordx4 (no VGPR
-// staging, no LDS write instructions): wave w fills the 1 KB blocks of 8 rows
-// number 8w..8w+7 of each operand, lane l landing at block + 16 l, i.e. row
-// (l >> 3) of the block, physical chunk (l & 7); the lane therefore fetches
-// logical chunk (l & 7) ^ swz(row).  Two stages live in four distinct LDS
-// arrays and the K loop is unrolled by two, so the stage written by the
-// in-flight loads is a different object from the one being read and no wait
-// on those loads is needed before the MFMA fragment reads.  Fragments are
-// double-buffered in registers: the LDS reads of substep s+1 are issued
-// before the 16 MFMAs of substep s.
-template <typename T>
-__device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0, char* la1,
-                                         char* lb1, floatx16 (&acc)[4][4]) {
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int nk = static_cast<int>((op.kbytes + kRowBytes - 1) / kRowBytes);
+// Buffer resource over a tile's operand.  Every offset used is below 2^31
+// (host limits), so 0x80000000 is always out of range: a lane given that
+// offset loads zeros, which is how ragged rows and K tails are filled.
+constexpr uint32_t kOob = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const char* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), static_cast<short>(0),
+                                           0x7FFFFFFF, 0x00020000);
+}
+#define MOE_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
+// acc += A_tile * B_tile^T over the whole K extent: 8 wavefronts in two
+// teams of four, one wave of each team per SIMD.  Team t computes tile rows
+// 128t..128t+127, its wave q columns 64q..64q+63 (gated forward: hidden units
+// 32q..32q+31, W1 then W3).  Each half K step (32 bf16) is a memory phase
+// (12 fragment reads, LDS -> registers) followed by an MFMA phase (16 MFMAs
+// from registers).  Team 1 runs one barrier behind team 0, so while one wave
+// of a SIMD issues MFMAs the other reads LDS.  Operand tiles go HBM -> LDS
+// with buffer_load ... lds (no register staging), issued by team 0 one step
+// ahead into the other of two stages.
+template <typename T, bool GATED, bool FULL>
+__device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0, char* la1,
+                                         char* lb1, floatx16 (&acc)[4][2]) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int team = wave >> 2, wq = wave & 3;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+  const int kbytes = op.kbytes;
+  const int nk = (kbytes + kRowBytes - 1) / kRowBytes;
   if (nk <= 0) return;
+  const int nk2 = (nk + 1) & ~1;   // odd counts load one all-zero step
 
-  // Wave w fills operand rows 64w .. 64w+63: block i (8 rows) of the wave
-  // covers rows 64w + 8i + (lane >> 3).  swz() of those rows only depends on
-  // the parity of i, so a full tile needs one row pointer per operand and two
-  // chunk offsets; ragged tiles (an expert's last rows, an N or K tail) take
-  // a path that clamps rows to valid ones and reads K-tail chunks as zeros.
-  const int lrow = wave * 64 + (lane >> 3);                 // block-0 row of this lane
-  const int coff0 = ((lane & 7) ^ swz(lrow)) * 16;           // even blocks
-  const int coff1 = ((lane & 7) ^ swz(lrow + 8)) * 16;       // odd blocks
-  const char* arow = op.a + static_cast<int64_t>(lrow) * op.lda;
-  const char* brow = (wave < 2 ? op.b_lo + static_cast<int64_t>(lrow) * op.ldb
-                               : op.b_hi + static_cast<int64_t>(lrow - 128) * op.ldb);
-  const bool full_rows = op.a_rows >= BM && op.b_rows_lo >= 128 && op.b_rows_hi >= 128;
-  const char* zero = reinterpret_cast<const char*>(g_zero_chunk);
-  auto dma = [&](int kt, char* sa, char* sb) {
-    const int64_t kofs = static_cast<int64_t>(kt) * kRowBytes;
-    if (full_rows && kofs + kRowBytes <= op.kbytes) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int blk = wave * 8 + i;
-        const int co = (i & 1) ? coff1 : coff0;
-        const char* ga = arow + i * 8 * op.lda + co + kofs;
-        const char* gb = brow + i * 8 * op.ldb + co + kofs;
-        __builtin_amdgcn_global_load_lds(ga, (__attribute__((address_space(3))) void*)(sa + blk * 1024), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(gb, (__attribute__((address_space(3))) void*)(sb + blk * 1024), 16, 0, 0);
-      }
-      return;
-    }
+  // Loads: 8-row block blk of an operand, lane l -> tile row blk*8 + (l >> 3),
+  // physical chunk l & 7, logical chunk (l & 7) ^ swz(row), which depends on
+  // the parity of blk only.
+  const int l3 = lane >> 3;
+  const int co0 = ((lane & 7) ^ swz(l3)) * 16, co1 = ((lane & 7) ^ swz(l3 + 8)) * 16;
+  const uint32_t la_row = static_cast<uint32_t>(l3 * op.lda);
+  const uint32_t lb_row = static_cast<uint32_t>(l3 * op.ldb);
+  const __amdgpu_buffer_rsrc_t ra = tile_rsrc(op.a);
+  const __amdgpu_buffer_rsrc_t rb = tile_rsrc(op.b);
+  const __amdgpu_buffer_rsrc_t rb3 = tile_rsrc(GATED ? op.b3 : op.b);
+  const int lda = static_cast<int>(op.lda), ldb = static_cast<int>(op.ldb);
+  // FULL: every row valid and K a whole number of steps, so a step is either
+  // entirely inside K or (the padding step) entirely outside.  Otherwise
+  // each lane checks its row and its K chunk.
+  auto load = [&](int kt, char* sa, char* sb, int b0, int nb) {
+    const int kofs = kt * kRowBytes;
+    const bool kin = kofs < kbytes;   // wave-uniform
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int blk = wave * 8 + i;
-      const int row = lrow + i * 8;
-      const int co = (i & 1) ? coff1 : coff0;
-      const bool kok = kofs + co < op.kbytes;
-      const char* ga = op.a + static_cast<int64_t>(min(row, op.a_rows - 1)) * op.lda;
-      const char* gb;
-      if (row < 128) {
-        gb = op.b_lo + static_cast<int64_t>(min(row, op.b_rows_lo - 1)) * op.ldb;
-      } else if (op.b_rows_hi > 0) {
-        gb = op.b_hi + static_cast<int64_t>(min(row - 128, op.b_rows_hi - 1)) * op.ldb;
-      } else {
-        gb = op.b_lo;   // rows past N: any valid row, their outputs are not stored
+      if (i < nb) {
+        const int blk = b0 + i;
+        const int co = (i & 1) ? co1 : co0;   // b0 is even
+        // B row of this block: plain, or W1/W3 groups of 32 (gated forward)
+        const int brow0 = GATED ? (blk >> 3) * 32 + (blk & 3) * 8 : blk * 8;
+        uint32_t oa = la_row + co, ob = lb_row + co;
+        if constexpr (FULL) {
+          if (!kin) oa = ob = kOob;
+        } else {
+          const bool kok = kofs + co < kbytes;
+          if (!kok || blk * 8 + l3 >= op.a_rows) oa = kOob;
+          if (!kok || brow0 + l3 >= op.b_rows) ob = kOob;
+        }
+        const int sa_off = blk * 8 * lda + kofs;
+        const int sb_off = brow0 * ldb + kofs;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, MOE_LDS(sa + blk * 1024), 16, oa, sa_off, 0, 0);
+        if (GATED && ((blk >> 2) & 1))
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rb3, MOE_LDS(sb + blk * 1024), 16, ob, sb_off, 0, 0);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, MOE_LDS(sb + blk * 1024), 16, ob, sb_off, 0, 0);
       }
-      ga = kok ? ga + co + kofs : zero;
-      gb = kok ? gb + co + kofs : zero;
-      __builtin_amdgcn_global_load_lds(ga, (__attribute__((address_space(3))) void*)(sa + blk * 1024), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(gb, (__attribute__((address_space(3))) void*)(sb + blk * 1024), 16, 0, 0);
-    }
-  };
-  const int fr_row = lane & 31;
-  const int fr_base_a = (wm * 128 + fr_row) * kRowBytes;
-  const int fr_base_b = (wn * 128 + fr_row) * kRowBytes;
-  uint4 fa[2][4], fb[2][4];
-  auto fread = [&](const char* sa, const char* sb, int s, int buf) {
-    const int sw = (((2 * s + (lane >> 5)) ^ swz(fr_row)) << 4);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      fa[buf][i] = *reinterpret_cast<const uint4*>(sa + fr_base_a + i * 32 * kRowBytes + sw);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      fb[buf][j] = *reinterpret_cast<const uint4*>(sb + fr_base_b + j * 32 * kRowBytes + sw);
-  };
-  auto mma = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) Mma<T>::run(acc[i][j], fa[buf][i], fb[buf][j]);
-  };
-  auto tile = [&](const char* sa, const char* sb) {
-    fread(sa, sb, 0, 0);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      if (s < 3) fread(sa, sb, s + 1, (s + 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
-      mma(s & 1);
-      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // K tiles in pairs (stage 0, then stage 1).  An odd count is rounded up:
-  // the extra tile lies past K and is loaded as zeros, adding nothing.  (One
-  // loop body and no peeled tail keeps the accumulators in place.)
-  const int nk2 = (nk + 1) & ~1;
-  dma(0, la0, lb0);
+  const int fr_row = lane & 31;
+  const int fr_a = (team * 128 + fr_row) * kRowBytes;
+  const int fr_b = (wq * 64 + fr_row) * kRowBytes;
+  uint4 fa[4][2], fb[2][2];   // [sub-tile][k sub-step within the half step]
+  // fragments of k sub-steps 2h and 2h+1 (one half of a K step)
+  auto fread = [&](const char* sa, const char* sb, int h) {
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int sw = ((4 * h + 2 * s2 + (lane >> 5)) ^ swz(fr_row)) << 4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        fa[i][s2] = *reinterpret_cast<const uint4*>(sa + fr_a + i * 32 * kRowBytes + sw);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        fb[j][s2] = *reinterpret_cast<const uint4*>(sb + fr_b + j * 32 * kRowBytes + sw);
+    }
+  };
+  auto mma = [&]() {
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) Mma<T>::run(acc[i][j], fa[i][s2], fb[j][s2]);
+  };
+  // s_waitcnt immediates (gfx9 encoding)
+  constexpr int kWaitVm0 = 0x0F70;    // vmcnt(0)
+  constexpr int kWaitLgkm0 = 0xC07F;  // lgkmcnt(0)
+  // one ping-pong phase pair: read half h of a stage, then its 16 MFMAs
+  auto half = [&](const char* sa, const char* sb, int h, bool wait_loads) {
+    fread(sa, sb, h);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    mma();
+    __builtin_amdgcn_sched_barrier(0);
+    if (wait_loads) __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    __builtin_amdgcn_s_barrier();
+  };
+
+  load(0, la0, lb0, wave * 4, 4);    // stage 0: all eight waves
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
-  for (int kt = 0; kt < nk2; kt += 2) {
-    dma(kt + 1, la1, lb1);
-    tile(la0, lb0);
-    __syncthreads();
-    if (kt + 2 < nk2) dma(kt + 2, la0, lb0);
-    tile(la1, lb1);
-    __syncthreads();
+  if (team == 0) {
+    // team 0 also loads stage kt+1 at the start of step kt and waits for it
+    // at the end of the step, four phases later
+    for (int kt = 0; kt < nk2; kt += 2) {
+      load(kt + 1, la1, lb1, wq * 8, 8);
+      half(la0, lb0, 0, false);
+      half(la0, lb0, 1, true);
+      if (kt + 2 < nk2) load(kt + 2, la0, lb0, wq * 8, 8);
+      half(la1, lb1, 0, false);
+      half(la1, lb1, 1, true);
+    }
+    __builtin_amdgcn_s_barrier();
+  } else {
+    __builtin_amdgcn_s_barrier();
+    for (int kt = 0; kt < nk2; kt += 2) {
+      half(la0, lb0, 0, false);
+      half(la0, lb0, 1, false);
+      half(la1, lb1, 0, false);
+      half(la1, lb1, 1, false);
+    }
   }
+  // every wave has passed the last barrier after its last LDS read: the
+  // operand buffers are free
 }
 
-// Stage rows [16h, 16h+16) of accumulator row-block i (32 rows) as fp32: the
-// lane's registers q in [8h, 8h+8) hold those rows.
-__device__ __forceinline__ void stage_strip(float* strip, const floatx16 (&acc)[4][4], int i,
+// Stage rows [16h, 16h+16) of the wave's accumulator row-block i (32 rows x
+// 64 columns) as fp32, row pitch kStripPitch: the lane's registers q in
+// [8h, 8h+8) hold those rows.
+__device__ __forceinline__ void stage_strip(float* strip, const floatx16 (&acc)[4][2], int i,
                                             int h) {
   const int lane = threadIdx.x & 63;
   const int half = lane >> 5, col = lane & 31;
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int q = 8 * h; q < 8 * h + 8; ++q) {
       const int row = ((q >> 2) - 2 * h) * 8 + half * 4 + (q & 3);
@@ -399,28 +424,43 @@ enum Pass { P_FWD_H = 0, P_FWD_Y = 1, P_BWD_DA = 2, P_BWD_DX = 3, P_BWD_DW2 = 4,
 template <typename T, int MODE, int PASS>
 __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams p) {
   // two stages of the A and B tiles, four distinct objects (see mainloop);
-  // after the K loop the same memory stages the epilogue
+  // after the K loop the same memory holds each wave's epilogue strips
   __shared__ __attribute__((aligned(16))) char la0[kTileBytes];
   __shared__ __attribute__((aligned(16))) char lb0[kTileBytes];
   __shared__ __attribute__((aligned(16))) char la1[kTileBytes];
   __shared__ __attribute__((aligned(16))) char lb1[kTileBytes];
   constexpr int ES = sizeof(T);
   constexpr bool VARK = MODE == M_DW;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int team = wave >> 2, wq = wave & 3;
   const Sched& sc = *p.sched;
   const int n_items = VARK ? sc.n_segs * p.mtiles_out * p.ntiles : sc.n_mtiles * p.ntiles;
   const int G = gridDim.x;
   const int lbase = (blockIdx.x % kXcds) * (G / kXcds) + blockIdx.x / kXcds;
+  // the wave's two staging strips (kStripsPerArray per 32 KB array)
+  auto strip_at = [&](int sidx) {
+    const int arr = sidx / kStripsPerArray, off = (sidx % kStripsPerArray) * kStripBytes;
+    char* base = arr == 0 ? la0 : (arr == 1 ? lb0 : la1);
+    return reinterpret_cast<float*>(base + off);
+  };
 
   for (int round = 0;; ++round) {
     const int L = round * G + lbase;
     if (L >= n_items) break;
+    // An opaque zero, produced inside the tile loop: the per-lane epilogue
+    // addresses derived from it are computed per tile instead of being
+    // hoisted out of the loop and held (or spilled) across the K loop.
+    int z;
+    asm volatile("s_mov_b32 %0, 0" : "=s"(z));
+    float* strip = strip_at(2 * wave) + z;
+    float* strip3 = strip_at(2 * wave + 1) + z;
     TileOps op;
     int g, row0, m_valid;       // var-M: expert, first global row, valid rows in tile
     int n0;                      // first output column of the tile
     int local_m0 = 0;            // var-M: first expert-local row
     int slot = -1, mt, nt;
+    op.b3 = nullptr;
     if constexpr (!VARK) {
       int mti;
       decode_grouped(L, sc.n_mtiles, p.ntiles, mti, nt);
@@ -432,21 +472,18 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
       op.a = p.A + static_cast<int64_t>(row0) * p.lda;
       op.lda = p.lda;
       op.a_rows = m_valid;
-      op.kbytes = p.kbytes;
+      op.kbytes = static_cast<int>(p.kbytes);
       op.ldb = p.ldb;
       const char* bg = p.B + static_cast<int64_t>(g) * p.b_gstride;
       if constexpr (MODE == M_FWD1_SWIGLU) {
-        n0 = nt * 128;  // f columns covered by this tile (W1 half + W3 half)
-        const char* b3 = p.B2 + static_cast<int64_t>(g) * p.b_gstride;
-        op.b_lo = bg + static_cast<int64_t>(n0) * p.ldb;
-        op.b_hi = b3 + static_cast<int64_t>(n0) * p.ldb;
-        op.b_rows_lo = op.b_rows_hi = min(128, p.N - n0);
+        n0 = nt * (BN / 2);  // hidden units covered by this tile (W1 and W3 rows)
+        op.b = bg + static_cast<int64_t>(n0) * p.ldb;
+        op.b3 = p.B2 + static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0) * p.ldb;
+        op.b_rows = min(BN / 2, p.N - n0);
       } else {
         n0 = nt * BN;
-        op.b_lo = bg + static_cast<int64_t>(n0) * p.ldb;
-        op.b_hi = op.b_lo + 128 * p.ldb;
-        op.b_rows_lo = min(128, p.N - n0);
-        op.b_rows_hi = min(128, p.N - n0 - 128);
+        op.b = bg + static_cast<int64_t>(n0) * p.ldb;
+        op.b_rows = min(BN, p.N - n0);
       }
     } else {
       const int tmn = p.mtiles_out * p.ntiles;
@@ -463,47 +500,39 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
       op.lda = p.lda;
       op.a_rows = m_valid;
       op.ldb = p.ldb;
-      op.b_lo = p.B + static_cast<int64_t>(n0) * p.ldb + static_cast<int64_t>(col) * ES;
-      op.b_hi = op.b_lo + 128 * p.ldb;
-      op.b_rows_lo = min(128, p.N - n0);
-      op.b_rows_hi = min(128, p.N - n0 - 128);
-      op.kbytes = static_cast<int64_t>(sg.z - sg.y) * ES;
+      op.b = p.B + static_cast<int64_t>(n0) * p.ldb + static_cast<int64_t>(col) * ES;
+      op.b_rows = min(BN, p.N - n0);
+      op.kbytes = (sg.z - sg.y) * ES;
     }
 
-    floatx16 acc[4][4];
-    mainloop<T>(op, la0, lb0, la1, lb1, acc);
-    // (the K loop ended with a barrier: the operand buffers are free)
+    floatx16 acc[4][2];
+    constexpr bool GATED = MODE == M_FWD1_SWIGLU;
+    if (op.a_rows >= BM && op.b_rows >= (GATED ? BN / 2 : BN) && op.kbytes % kRowBytes == 0)
+      mainloop<T, GATED, true>(op, la0, lb0, la1, lb1, acc);
+    else
+      mainloop<T, GATED, false>(op, la0, lb0, la1, lb1, acc);
 
-    // staging strips: wave w uses (w < 2 ? la0 : lb0) + (w & 1) * kStripBytes,
-    // and a second strip at the same place in la1 / lb1
-    auto strip_of = [&](int w) {
-      return reinterpret_cast<float*>((w < 2 ? la0 : lb0) + (w & 1) * kStripBytes);
-    };
-    float* strip = strip_of(wave);
-    float* strip3 = reinterpret_cast<float*>((wave < 2 ? la1 : lb1) + (wave & 1) * kStripBytes);
-
+    // Epilogue, wave by wave: 16 accumulator rows at a time go through the
+    // wave's own LDS strip, then each lane finishes 8 consecutive columns of
+    // a row and writes them as one vector.
+    const int wcol = wq * 64;   // the wave's first tile column
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      stage_strip(strip, acc, i >> 1, i & 1);
-      __syncthreads();
-      const int srow0 = wm * 128 + i * kStripRows;  // strip's first row within the tile
-      if constexpr (MODE == M_FWD1_SWIGLU) {
-        // waves (wm,0) hold H1, (wm,1) hold H3 for the same columns; each of
-        // the pair finishes 8 of the strip's 16 rows
-        const float* s1 = strip_of(wm * 2 + 0);
-        const float* s3 = strip_of(wm * 2 + 1);
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-        for (int it = 0; it < 2; ++it) {
-          const int r = wn * 8 + it * 4 + (lane >> 4);
-          const int c8 = (lane & 15) * 8;
+      for (int h = 0; h < 2; ++h) {
+        stage_strip(strip, acc, i, h);
+        const int srow0 = team * 128 + i * 32 + h * 16;  // strip's first row within the tile
+        if constexpr (MODE == M_FWD1_SWIGLU) {
+          // strip columns [0,32): H1, [32,64): H3 of hidden units n0 + 32wq + c
+          const int r = lane >> 2, c8 = (lane & 3) * 8;
           const int lm = srow0 + r;
-          const int gc = n0 + c8;
+          const int gc = n0 + wq * 32 + c8;
           if (lm < m_valid && gc < p.N) {
             float h1[8], h3[8], a[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-              h1[e] = Elem<T>::to_f(Elem<T>::from_f(s1[r * kStripPitch + c8 + e]));
-              h3[e] = Elem<T>::to_f(Elem<T>::from_f(s3[r * kStripPitch + c8 + e]));
+              h1[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kStripPitch + c8 + e]));
+              h3[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kStripPitch + 32 + c8 + e]));
               a[e] = h1[e] * sigm(h1[e]) * h3[e];
             }
             const int64_t grow = row0 + lm;
@@ -513,126 +542,121 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
             }
             store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, a);
           }
-        }
-      } else if constexpr (MODE == M_FWD1 || MODE == M_STORE) {
+        } else if constexpr (MODE == M_FWD1 || MODE == M_STORE) {
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-          const int r = it * 4 + (lane >> 4);
-          const int c8 = (lane & 15) * 8;
-          const int lm = srow0 + r;
-          const int gc = n0 + wn * 128 + c8;
-          if (lm < m_valid && gc < p.N) {
-            float v[8];
+          for (int it = 0; it < 2; ++it) {
+            const int r = it * 8 + (lane >> 3), c8 = (lane & 7) * 8;
+            const int lm = srow0 + r;
+            const int gc = n0 + wcol + c8;
+            if (lm < m_valid && gc < p.N) {
+              float v[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] = strip[r * kStripPitch + c8 + e];
-            const int64_t grow = row0 + lm;
-            if constexpr (MODE == M_FWD1) {
-              float h[8];
+              for (int e = 0; e < 8; ++e) v[e] = strip[r * kStripPitch + c8 + e];
+              const int64_t grow = row0 + lm;
+              if constexpr (MODE == M_FWD1) {
+                float hh[8];
 #pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                h[e] = Elem<T>::to_f(Elem<T>::from_f(v[e]));
-                v[e] = act_f(h[e], p.act);
+                for (int e = 0; e < 8; ++e) {
+                  hh[e] = Elem<T>::to_f(Elem<T>::from_f(v[e]));
+                  v[e] = act_f(hh[e], p.act);
+                }
+                if (p.H1) store_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, hh);
               }
-              if (p.H1) store_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h);
-            }
-            store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, v);
-          }
-        }
-      } else if constexpr (MODE == M_BWD_DA || MODE == M_BWD_DA_SWIGLU) {
-        constexpr bool SW = MODE == M_BWD_DA_SWIGLU;
-#pragma unroll
-        for (int it = 0; it < 4; ++it) {
-          const int r = it * 4 + (lane >> 4);
-          const int c8 = (lane & 15) * 8;
-          const int lm = srow0 + r;
-          const int gc = n0 + wn * 128 + c8;
-          float g1[8], g3[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) g1[e] = g3[e] = 0.f;
-          if (lm < m_valid && gc < p.N) {
-            const int64_t grow = row0 + lm;
-            float h1[8];
-            load_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h1);
-            if constexpr (SW) {
-              float h3[8];
-              load_vec<T>(p.H3 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h3);
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                const float da = strip[r * kStripPitch + c8 + e];
-                const float sg = sigm(h1[e]);
-                g1[e] = Elem<T>::to_f(Elem<T>::from_f(da * h3[e] * sg * (1.f + h1[e] * (1.f - sg))));
-                g3[e] = Elem<T>::to_f(Elem<T>::from_f(da * h1[e] * sg));
-              }
-              store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
-              store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(p.f + gc) * ES, g3);
-            } else {
-#pragma unroll
-              for (int e = 0; e < 8; ++e)
-                g1[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kStripPitch + c8 + e] *
-                                                       act_grad_f(h1[e], p.act)));
-              store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
+              store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, v);
             }
           }
-          // keep the rounded gradients for the transposed store (in place:
-          // each lane rewrites exactly the elements it read); rows past the
-          // expert's rows become zero (the transposed buffers are zero-padded)
+        } else if constexpr (MODE == M_BWD_DA || MODE == M_BWD_DA_SWIGLU) {
+          constexpr bool SW = MODE == M_BWD_DA_SWIGLU;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            strip[r * kStripPitch + c8 + e] = g1[e];
-            if constexpr (SW) strip3[r * kStripPitch + c8 + e] = g3[e];
+          for (int it = 0; it < 2; ++it) {
+            const int r = it * 8 + (lane >> 3), c8 = (lane & 7) * 8;
+            const int lm = srow0 + r;
+            const int gc = n0 + wcol + c8;
+            float g1[8], g3[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) g1[e] = g3[e] = 0.f;
+            if (lm < m_valid && gc < p.N) {
+              const int64_t grow = row0 + lm;
+              float h1[8];
+              load_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h1);
+              if constexpr (SW) {
+                float h3[8];
+                load_vec<T>(p.H3 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h3);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                  const float da = strip[r * kStripPitch + c8 + e];
+                  const float sg = sigm(h1[e]);
+                  g1[e] = Elem<T>::to_f(Elem<T>::from_f(da * h3[e] * sg * (1.f + h1[e] * (1.f - sg))));
+                  g3[e] = Elem<T>::to_f(Elem<T>::from_f(da * h1[e] * sg));
+                }
+                store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
+                store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(p.f + gc) * ES, g3);
+              } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                  g1[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kStripPitch + c8 + e] *
+                                                         act_grad_f(h1[e], p.act)));
+                store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
+              }
+            }
+            // keep the rounded gradients for the transposed store (in place:
+            // each lane rewrites exactly the elements it read); rows past the
+            // expert's rows become zero (the transposed buffers are zero-padded)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              strip[r * kStripPitch + c8 + e] = g1[e];
+              if constexpr (SW) strip3[r * kStripPitch + c8 + e] = g3[e];
+            }
           }
-        }
-        __syncthreads();
-        // transposed store: 8 consecutive expert rows of one column per lane
-        const int kcol0 = sc.kbase[g] + local_m0 + srow0;   // first transposed column
-        const int kpad_g = (sc.rows[g] + kTT - 1) / kTT * kTT;
+          // transposed store: 8 consecutive expert rows of one column per lane
+          const int kcol0 = sc.kbase[g] + local_m0 + srow0;   // first transposed column
+          const int kpad_g = (sc.rows[g] + kTT - 1) / kTT * kTT;
+          const int gc = n0 + wcol + lane;
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-          const int c = it * 32 + (lane >> 1);
-          const int rg = (lane & 1) * 8;
-          const int gc = n0 + wn * 128 + c;
-          if (gc < p.N && local_m0 + srow0 + rg < kpad_g) {
-            float v[8];
+          for (int it = 0; it < 2; ++it) {
+            const int rg = it * 8;
+            if (gc < p.N && local_m0 + srow0 + rg < kpad_g) {
+              float v[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] = strip[(rg + e) * kStripPitch + c];
-            store_vec<T>(p.CT + static_cast<int64_t>(gc) * p.ldct +
-                             static_cast<int64_t>(kcol0 + rg) * ES, v);
-            if constexpr (SW) {
-#pragma unroll
-              for (int e = 0; e < 8; ++e) v[e] = strip3[(rg + e) * kStripPitch + c];
-              store_vec<T>(p.CT + static_cast<int64_t>(p.f + gc) * p.ldct +
+              for (int e = 0; e < 8; ++e) v[e] = strip[(rg + e) * kStripPitch + lane];
+              store_vec<T>(p.CT + static_cast<int64_t>(gc) * p.ldct +
                                static_cast<int64_t>(kcol0 + rg) * ES, v);
+              if constexpr (SW) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = strip3[(rg + e) * kStripPitch + lane];
+                store_vec<T>(p.CT + static_cast<int64_t>(p.f + gc) * p.ldct +
+                                 static_cast<int64_t>(kcol0 + rg) * ES, v);
+              }
             }
           }
-        }
-      } else {  // M_DW: fp32 rows of dW (or of a partial-sum slot)
+        } else {  // M_DW: fp32 rows of dW (or of a partial-sum slot)
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-          const int r = it * 4 + (lane >> 4);
-          const int c8 = (lane & 15) * 8;
-          const int lm = srow0 + r;
-          const int gc = n0 + wn * 128 + c8;
-          if (lm < m_valid && gc < p.N) {
-            const int orow = row0 + lm;
-            float* dst;
-            if (slot >= 0) {
-              dst = p.partial + static_cast<int64_t>(slot) * p.slot_elems +
-                    static_cast<int64_t>(orow) * p.N + gc;
-            } else if (orow < p.split_row) {
-              dst = p.dwA + static_cast<int64_t>(g) * p.dw_gstride +
-                    static_cast<int64_t>(orow) * p.N + gc;
-            } else {
-              dst = p.dwB + static_cast<int64_t>(g) * p.dw_gstride +
-                    static_cast<int64_t>(orow - p.split_row) * p.N + gc;
+          for (int it = 0; it < 2; ++it) {
+            const int r = it * 8 + (lane >> 3), c8 = (lane & 7) * 8;
+            const int lm = srow0 + r;
+            const int gc = n0 + wcol + c8;
+            if (lm < m_valid && gc < p.N) {
+              const int orow = row0 + lm;
+              float* dst;
+              if (slot >= 0) {
+                dst = p.partial + static_cast<int64_t>(slot) * p.slot_elems +
+                      static_cast<int64_t>(orow) * p.N + gc;
+              } else if (orow < p.split_row) {
+                dst = p.dwA + static_cast<int64_t>(g) * p.dw_gstride +
+                      static_cast<int64_t>(orow) * p.N + gc;
+              } else {
+                dst = p.dwB + static_cast<int64_t>(g) * p.dw_gstride +
+                      static_cast<int64_t>(orow - p.split_row) * p.N + gc;
+              }
+              const float* sp = strip + r * kStripPitch + c8;
+              *reinterpret_cast<float4*>(dst) = make_float4(sp[0], sp[1], sp[2], sp[3]);
+              *reinterpret_cast<float4*>(dst + 4) = make_float4(sp[4], sp[5], sp[6], sp[7]);
             }
-            const float* sp = strip + r * kStripPitch + c8;
-            *reinterpret_cast<float4*>(dst) = make_float4(sp[0], sp[1], sp[2], sp[3]);
-            *reinterpret_cast<float4*>(dst + 4) = make_float4(sp[4], sp[5], sp[6], sp[7]);
           }
         }
       }
-      __syncthreads();
     }
+    __syncthreads();   // strips are free before the next tile's loads
   }
 }
 
@@ -785,7 +809,12 @@ bool make_plan(moe_dtype dt, moe_act act, int E, int d, int f, int64_t rows_allo
   pl.max_mtiles = cdiv(rows_alloc, BM) + E;
   pl.max_ttiles = cdiv(rows_alloc, kTT) + E;
   const int64_t kcap = (rows_alloc + kTT - 1) / kTT * kTT + static_cast<int64_t>(kTT) * E;
-  if (kcap >= (int64_t(1) << 31)) return false;
+  // every GEMM operand offset inside a 256-row tile stays below 2^31 bytes
+  // (buffer-resource loads with 32-bit offsets)
+  int64_t max_ld = kcap;
+  if (2 * static_cast<int64_t>(f) > max_ld) max_ld = 2 * static_cast<int64_t>(f);
+  if (d > max_ld) max_ld = d;
+  if (max_ld * static_cast<int64_t>(pl.es) > kMaxOperandRowBytes) return false;
   pl.kpad_cap = static_cast<int>(kcap);
   const int tmn2 = cdiv(d, BM) * cdiv(f, BN);
   const int tmn13 = cdiv(pl.F, BM) * cdiv(d, BN);
