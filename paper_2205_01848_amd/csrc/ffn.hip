@@ -719,13 +719,15 @@ __global__ __launch_bounds__(256) void rows_transpose_kernel(
   }
 }
 
-// out[g, c, co + r] = in[g, r, c] for in [E, R, C] (weights).
+// out[g, c, co + r] = in[g, r, c] for in [E, R, C] (weights), for the experts
+// that have rows (the others' transposed weights are never read).
 template <typename T>
 __global__ __launch_bounds__(256) void weight_transpose_kernel(
     const T* __restrict__ in, int R, int C, T* __restrict__ out, int64_t ld_out, int co,
-    int64_t out_gstride) {
+    int64_t out_gstride, const Sched* __restrict__ sc) {
   __shared__ T tile[kTT][kTT + 1];
   const int g = blockIdx.z;
+  if (sc->rows[g] == 0) return;
   const int c0 = blockIdx.x * kTT, r0 = blockIdx.y * kTT;
   const T* src = in + static_cast<int64_t>(g) * R * C;
   T* dst = out + static_cast<int64_t>(g) * out_gstride;
@@ -916,16 +918,20 @@ moe_status launch_rows_transpose(hipStream_t s, moe_dtype dt, const FfnPlan& pl,
   return MOE_OK;
 }
 
-moe_status launch_weight_transpose(hipStream_t s, moe_dtype dt, const void* in, int E, int R,
-                                   int C, char* out, int64_t ld_out, int co, int64_t gstride) {
+moe_status launch_weight_transpose(hipStream_t s, moe_dtype dt, const FfnPlan& pl, char* ws,
+                                   const void* in, int E, int R, int C, char* out,
+                                   int64_t ld_out, int co, int64_t gstride) {
   dim3 grid(cdiv(C, kTT), cdiv(R, kTT), E);
+  const Sched* sc = reinterpret_cast<const Sched*>(ws + pl.o_sched);
   MOE_TIMED("transpose_weights", s);
   if (dt == MOE_BF16)
     weight_transpose_kernel<uint16_t><<<grid, 256, 0, s>>>(
-        static_cast<const uint16_t*>(in), R, C, reinterpret_cast<uint16_t*>(out), ld_out, co, gstride);
+        static_cast<const uint16_t*>(in), R, C, reinterpret_cast<uint16_t*>(out), ld_out, co,
+        gstride, sc);
   else
     weight_transpose_kernel<float><<<grid, 256, 0, s>>>(
-        static_cast<const float*>(in), R, C, reinterpret_cast<float*>(out), ld_out, co, gstride);
+        static_cast<const float*>(in), R, C, reinterpret_cast<float*>(out), ld_out, co, gstride,
+        sc);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }
@@ -1056,10 +1062,13 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   const char* h3 = sw ? h1 + rows_alloc * f * es : nullptr;
 
   // weights to K-contiguous form for the data-gradient products
-  MOE_TRY(launch_weight_transpose(s, dt, w2, E, d, f, w2t, d, 0, static_cast<int64_t>(f) * d));
-  MOE_TRY(launch_weight_transpose(s, dt, w1, E, f, d, w13t, F, 0, static_cast<int64_t>(d) * F));
+  MOE_TRY(launch_weight_transpose(s, dt, pl, ws, w2, E, d, f, w2t, d, 0,
+                                  static_cast<int64_t>(f) * d));
+  MOE_TRY(launch_weight_transpose(s, dt, pl, ws, w1, E, f, d, w13t, F, 0,
+                                  static_cast<int64_t>(d) * F));
   if (sw)
-    MOE_TRY(launch_weight_transpose(s, dt, w3, E, f, d, w13t, F, f, static_cast<int64_t>(d) * F));
+    MOE_TRY(launch_weight_transpose(s, dt, pl, ws, w3, E, f, d, w13t, F, f,
+                                    static_cast<int64_t>(d) * F));
 
   // dA = dY W2 -> dH (row-major and transposed)
   GemmParams p = base_params(pl, offsets, ws);
