@@ -21,6 +21,8 @@
 // per wavefront on its fp32 accumulators, staged 16 rows at a time through a
 // private LDS strip, and write 16-byte vectors.
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "validate.hpp"
 
@@ -42,7 +44,7 @@ static_assert(3 * kStripsPerArray >= 16, "two staging strips per wave in three o
 constexpr int kGroupM = 4;      // M tiles per scheduling group
 constexpr int kXcds = 8;
 constexpr int kSplitFloor = 512;  // smallest K chunk of a split dW product
-constexpr int kTT = 64;           // transpose tile
+constexpr int kKc = 64;           // split chunks are multiples of this many rows
 constexpr int64_t kMaxOperandRowBytes = (int64_t(1) << 23) - 64;  // 256 rows < 2^31 bytes
 
 enum Act { ACT_RELU = 0, ACT_GELU = 1, ACT_SWIGLU = 2 };
@@ -50,14 +52,10 @@ enum Act { ACT_RELU = 0, ACT_GELU = 1, ACT_SWIGLU = 2 };
 // Device-side schedule written by schedule_kernel.
 struct Sched {
   int n_mtiles;    // (expert, m0) tiles of BM rows
-  int n_ttiles;    // (expert, r0) tiles of 64 rows for the transposes
   int n_segs;      // (expert, k range) segments of the dW products
   int kc;          // split chunk (rows)
-  int kpad_total;  // columns used in the transposed buffers
   int n_slots;     // partial-sum slots used
-  int pad_[2];
   int rows[kMaxE];    // clamped rows per expert
-  int kbase[kMaxE];   // first column of expert e in the transposed buffers
   int slot0[kMaxE];   // first partial slot of expert e (split experts)
   int nsplit[kMaxE];  // K segments of expert e
 };
@@ -104,16 +102,17 @@ __device__ __forceinline__ float sigm(float h) { return 1.f / (1.f + expf(-h)); 
 // schedule
 // ---------------------------------------------------------------------------
 // One workgroup; thread 0 walks the experts in order.  Clamps every expert's
-// rows to its region and to rows_alloc, and the totals to the host bounds
+// rows to its region and to rows_alloc, and the tile count to the host bound
 // the workspace was sized for, so no later kernel can index out of bounds.
+// The weight-gradient products split an expert's rows into K segments only
+// when few experts carry most rows (about 512 work items over all of them).
 __global__ void schedule_kernel(const int32_t* __restrict__ offsets,
                                 const int32_t* __restrict__ rows, int E,
-                                int64_t rows_alloc, int max_mtiles, int max_ttiles,
-                                int kpad_cap, int max_segs, int tmn_min, int max_slots,
-                                Sched* __restrict__ s, int2* __restrict__ mtile,
-                                int2* __restrict__ ttile, int4* __restrict__ seg) {
+                                int64_t rows_alloc, int max_mtiles, int max_segs, int tmn_min,
+                                int max_slots, Sched* __restrict__ s, int2* __restrict__ mtile,
+                                int4* __restrict__ seg) {
   if (threadIdx.x != 0) return;
-  int nm = 0, nt = 0, kb = 0;
+  int nm = 0;
   int64_t kwork = 0;
   for (int g = 0; g < E; ++g) {
     const int64_t off = offsets[g];
@@ -122,31 +121,19 @@ __global__ void schedule_kernel(const int32_t* __restrict__ offsets,
     m = min(m, static_cast<int64_t>(offsets[g + 1]) - off);
     m = min(m, rows_alloc - off);
     m = max(m, int64_t(0));
-    // keep the tile lists and transposed columns inside their bounds
-    const int64_t room_m = static_cast<int64_t>(max_mtiles - nm) * BM;
-    const int64_t room_k = static_cast<int64_t>(kpad_cap - kb);
-    m = min(m, room_m);
-    m = min(m, room_k / kTT * kTT);
-    m = min(m, static_cast<int64_t>(max_ttiles - nt) * kTT);
+    m = min(m, static_cast<int64_t>(max_mtiles - nm) * BM);
     const int mi = static_cast<int>(m);
     s->rows[g] = mi;
     for (int m0 = 0; m0 < mi; m0 += BM) mtile[nm++] = make_int2(g, m0);
-    const int kp = (mi + kTT - 1) / kTT * kTT;
-    s->kbase[g] = kb;
-    for (int r0 = 0; r0 < kp; r0 += kTT) ttile[nt++] = make_int2(g, r0);
-    kb += kp;
-    kwork += kp;
+    kwork += (mi + kKc - 1) / kKc * kKc;
   }
   s->n_mtiles = nm;
-  s->n_ttiles = nt;
-  s->kpad_total = kb;
-  // K chunk: aim at about 2 x 256 work items over all split products
   int64_t kc = (kwork * tmn_min + 511) / 512;
-  kc = (kc + kTT - 1) / kTT * kTT;
+  kc = (kc + kKc - 1) / kKc * kKc;
   kc = max(kc, static_cast<int64_t>(kSplitFloor));
   int ns = 0, slots = 0;
   for (int g = 0; g < E; ++g) {
-    const int kp = (s->rows[g] + kTT - 1) / kTT * kTT;
+    const int kp = s->rows[g];
     int nsp = kp > kc ? static_cast<int>((kp + kc - 1) / kc) : 1;
     if (nsp > 1 && (slots + nsp > max_slots || ns + nsp > max_segs)) nsp = 1;
     if (ns + nsp > max_segs) nsp = 0;  // cannot happen with host bounds; stay in bounds
@@ -183,29 +170,46 @@ template <> struct Mma<float> {
   }
 };
 
-// One tile's operand description (byte pointers, byte strides).  Rows of a
-// tile at or past a_rows / b_rows, and K bytes at or past kbytes, read as 0.
+// Operand layouts.  Every product is C[m, n] = sum_k A[m, k] B[n, k]; an
+// operand is stored either K-contiguous (rows are m (or n), k along each
+// row: activations in the forward, weights as out x in) or K-major (rows are
+// k, m along each row: the weights in the data-gradient products, and both
+// operands of the weight-gradient products, which contract over the
+// dispatched rows).
+enum Layout { L_KC = 0, L_KM = 1 };
+
+// One operand of one tile (byte pointers, byte strides).
+//  KC: base = tile row 0 at k = 0; rows = valid tile rows.
+//  KM: base = k-row 0 at tile column 0; rows = valid tile columns; k-rows at
+//      or past `split` come from base2 (k counted from split), else base.
+//  Gated forward (KC B only): base holds the W1 rows, base2 the W3 rows.
+struct Operand {
+  const char* base;
+  const char* base2;
+  int64_t ld;         // bytes between consecutive rows
+  int rows;
+  int split;
+};
 struct TileOps {
-  const char* a;      // A tile: row 0, k = 0
-  int64_t lda;        // bytes between A rows
-  int a_rows;         // valid A rows
-  const char* b;      // B tile: row 0, k = 0
-  const char* b3;     // gated forward: the W3 rows (b holds W1), else null
-  int64_t ldb;
-  int b_rows;         // valid B rows (gated forward: valid hidden units)
-  int kbytes;         // K extent in bytes (multiple of 16)
+  Operand a, b;
+  int K;              // valid k values; rows / columns / k past the valid ones read as 0
 };
 
-// LDS tile layout: row r (0..255) of 128 bytes, its 16-byte chunk c stored at
+// KC LDS tile: row r (0..255) of 128 bytes, its 16-byte chunk c stored at
 // r*128 + ((c ^ ((r >> 1) & 7)) << 4).  gfx950 LDS serves 16 lanes of a
 // 16-byte access per cycle from 64 banks (256 bytes): the MFMA fragment reads
 // touch 16 consecutive rows at one logical chunk; rows alternate bank halves
 // and (r >> 1) & 7 spreads each half's 8 rows over its 8 slots.
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+// KM LDS tile: k-row r of 256 elements, its 32-element segment g stored at
+// segment g ^ (r & 3).  A transpose read takes, per 32-lane half, 4
+// consecutive k-rows of one 32-element segment (64 bytes of bf16 each); the
+// XOR puts those rows in 4 different quarters of the 256-byte bank space.
 
-// Buffer resource over a tile's operand.  Every offset used is below 2^31
-// (host limits), so 0x80000000 is always out of range: a lane given that
-// offset loads zeros, which is how ragged rows and K tails are filled.
+// Buffer resource over an operand.  Every offset used is below 2^31 (host
+// limits; K-major resources are re-based every K step), so 0x80000000 is
+// always out of range: a lane given that offset loads zeros, which is how
+// ragged rows, columns and K tails are filled.
 constexpr uint32_t kOob = 0x80000000u;
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const char* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), static_cast<short>(0),
@@ -213,18 +217,32 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const char* base) {
 }
 #define MOE_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
+typedef short v4s __attribute__((ext_vector_type(4)));
+// 4 bf16 of one k-row run, transposed across each 16-lane group (gfx950
+// ds_read_b64_tr_b16): lane i = 4a + b of a group gets element b of the run
+// addressed by lanes 4r + a, for r = 0..3.
+__device__ __forceinline__ uint2 read_tr(const char* p) {
+  const v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
 // acc += A_tile * B_tile^T over the whole K extent: 8 wavefronts in two
 // teams of four, one wave of each team per SIMD.  Team t computes tile rows
 // 128t..128t+127, its wave q columns 64q..64q+63 (gated forward: hidden units
 // 32q..32q+31, W1 then W3).  Each half K step (32 bf16) is a memory phase
-// (12 fragment reads, LDS -> registers) followed by an MFMA phase (16 MFMAs
-// from registers).  Team 1 runs one barrier behind team 0, so while one wave
-// of a SIMD issues MFMAs the other reads LDS.  Operand tiles go HBM -> LDS
-// with buffer_load ... lds (no register staging), issued by team 0 one step
-// ahead into the other of two stages.
-template <typename T, bool GATED, bool FULL>
+// (12 fragments, LDS -> registers) followed by an MFMA phase (16 MFMAs from
+// registers).  Team 1 runs one barrier behind team 0, so while one wave of a
+// SIMD issues MFMAs the other reads LDS.  Operand tiles go HBM -> LDS with
+// buffer_load ... lds (no register staging), issued by team 0 one step ahead
+// into the other of two stages.  FULL: every tile row and column is valid;
+// K tails are checked per step either way.
+template <typename T, int ALAY, int BLAY, bool GATED, bool FULL>
 __device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0, char* la1,
                                          char* lb1, floatx16 (&acc)[4][2]) {
+  constexpr int ES = sizeof(T);
+  constexpr int KSTEP = kRowBytes / ES;   // k values per step (KC: 128 bytes per row)
+  constexpr int KMR = 2 / (ES / 2);       // KM: k-rows per 1 KB block (bf16 2, fp32 1)
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int team = wave >> 2, wq = wave & 3;
@@ -234,69 +252,146 @@ __device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
-  const int kbytes = op.kbytes;
-  const int nk = (kbytes + kRowBytes - 1) / kRowBytes;
+  const int K = op.K;
+  const int nk = (K + KSTEP - 1) / KSTEP;
   if (nk <= 0) return;
   const int nk2 = (nk + 1) & ~1;   // odd counts load one all-zero step
 
-  // Loads: 8-row block blk of an operand, lane l -> tile row blk*8 + (l >> 3),
-  // physical chunk l & 7, logical chunk (l & 7) ^ swz(row), which depends on
-  // the parity of blk only.
+  // ---- loads.  A 1 KB load covers one 8-row block of a KC tile (lane l ->
+  // row 8 blk + (l >> 3), physical chunk l & 7, logical chunk (l & 7) ^
+  // swz(row), depending on the parity of blk only), or KMR k-rows of a KM
+  // tile (lane l -> k-row KMR blk + (l >> 5) (bf16) / blk (fp32), physical
+  // element e = 16 l / ES within the row, column = segment swizzled by k & 3).
   const int l3 = lane >> 3;
   const int co0 = ((lane & 7) ^ swz(l3)) * 16, co1 = ((lane & 7) ^ swz(l3 + 8)) * 16;
-  const uint32_t la_row = static_cast<uint32_t>(l3 * op.lda);
-  const uint32_t lb_row = static_cast<uint32_t>(l3 * op.ldb);
-  const __amdgpu_buffer_rsrc_t ra = tile_rsrc(op.a);
-  const __amdgpu_buffer_rsrc_t rb = tile_rsrc(op.b);
-  const __amdgpu_buffer_rsrc_t rb3 = tile_rsrc(GATED ? op.b3 : op.b);
-  const int lda = static_cast<int>(op.lda), ldb = static_cast<int>(op.ldb);
-  // FULL: every row valid and K a whole number of steps, so a step is either
-  // entirely inside K or (the padding step) entirely outside.  Otherwise
-  // each lane checks its row and its K chunk.
+  const int kr = ES == 2 ? lane >> 5 : 0;                       // KM k-row within the block
+  const int pe = ES == 2 ? (lane & 31) * 8 : lane * 4;          // KM physical element
+  // KM column of the lane for k-row residue q = k & 3
+  auto km_col = [&](int q) { return (((pe >> 5) ^ q) << 5) + (pe & 31); };
+  auto ld_of = [&](const Operand& o) { return static_cast<int>(o.ld); };
+
+  // one operand, one block, one K step.  rs/rs2: resources (KM: of this step)
+  auto load_op = [&](auto lay, const Operand& o, const __amdgpu_buffer_rsrc_t& rs,
+                     const __amdgpu_buffer_rsrc_t& rs2, char* dst, int blk, int kt, bool kfull,
+                     bool kany, bool gated) {
+    constexpr int LAY = decltype(lay)::value;
+    uint32_t off;
+    int soff;
+    bool second = false;
+    if constexpr (LAY == L_KC) {
+      const int co = (blk & 1) ? co1 : co0;
+      // gated forward: W1/W3 groups of 32 rows
+      const int row0 = gated ? (blk >> 3) * 32 + (blk & 3) * 8 : blk * 8;
+      second = gated && ((blk >> 2) & 1);
+      off = static_cast<uint32_t>(l3 * ld_of(o)) + co;
+      soff = row0 * ld_of(o) + kt * kRowBytes;
+      if (!FULL || !kfull) {
+        const bool ok = (FULL || row0 + l3 < o.rows) && (kfull || kt * kRowBytes + co < K * ES);
+        if (!ok) off = kOob;
+      }
+    } else {
+      const int krel = KMR * blk;                  // first k-row of the block in the step
+      const int kabs = kt * KSTEP + krel;
+      const int q = (krel + kr) & 3;               // k & 3 (steps are multiples of 4 rows)
+      const int col = km_col(q);
+      second = kabs >= o.split;
+      off = static_cast<uint32_t>(kr * ld_of(o) + col * ES);
+      soff = krel * ld_of(o);
+      if (!FULL || !kfull) {
+        const bool ok = (FULL || col < o.rows) && (kfull || kabs + kr < K);
+        if (!ok) off = kOob;
+      }
+    }
+    if (!kany) off = kOob;
+    if (second)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs2, MOE_LDS(dst + blk * 1024), 16, off, soff, 0, 0);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, MOE_LDS(dst + blk * 1024), 16, off, soff, 0, 0);
+  };
+  using KC_ = std::integral_constant<int, L_KC>;
+  using KM_ = std::integral_constant<int, L_KM>;
+  // resources: KC operands over the whole tile, KM operands re-based per step
+  const __amdgpu_buffer_rsrc_t ra_t = tile_rsrc(op.a.base);
+  const __amdgpu_buffer_rsrc_t rb_t = tile_rsrc(op.b.base);
+  const __amdgpu_buffer_rsrc_t rb3_t = tile_rsrc(GATED ? op.b.base2 : op.b.base);
+  auto km_rsrc = [&](const Operand& o, int kt, bool second) {
+    const int64_t k = static_cast<int64_t>(kt) * KSTEP - (second ? o.split : 0);
+    return tile_rsrc((second ? o.base2 : o.base) + k * o.ld);
+  };
   auto load = [&](int kt, char* sa, char* sb, int b0, int nb) {
-    const int kofs = kt * kRowBytes;
-    const bool kin = kofs < kbytes;   // wave-uniform
+    const bool kfull = (kt + 1) * KSTEP <= K;   // wave-uniform
+    const bool kany = kt * KSTEP < K;
+    __amdgpu_buffer_rsrc_t ra = ra_t, ra2 = ra_t, rb = rb_t, rb2 = rb3_t;
+    if constexpr (ALAY == L_KM) {
+      ra = km_rsrc(op.a, kt, false);
+      ra2 = op.a.base2 ? km_rsrc(op.a, kt, true) : ra;
+    }
+    if constexpr (BLAY == L_KM) {
+      rb = km_rsrc(op.b, kt, false);
+      rb2 = op.b.base2 ? km_rsrc(op.b, kt, true) : rb;
+    }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       if (i < nb) {
-        const int blk = b0 + i;
-        const int co = (i & 1) ? co1 : co0;   // b0 is even
-        // B row of this block: plain, or W1/W3 groups of 32 (gated forward)
-        const int brow0 = GATED ? (blk >> 3) * 32 + (blk & 3) * 8 : blk * 8;
-        uint32_t oa = la_row + co, ob = lb_row + co;
-        if constexpr (FULL) {
-          if (!kin) oa = ob = kOob;
-        } else {
-          const bool kok = kofs + co < kbytes;
-          if (!kok || blk * 8 + l3 >= op.a_rows) oa = kOob;
-          if (!kok || brow0 + l3 >= op.b_rows) ob = kOob;
-        }
-        const int sa_off = blk * 8 * lda + kofs;
-        const int sb_off = brow0 * ldb + kofs;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, MOE_LDS(sa + blk * 1024), 16, oa, sa_off, 0, 0);
-        if (GATED && ((blk >> 2) & 1))
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rb3, MOE_LDS(sb + blk * 1024), 16, ob, sb_off, 0, 0);
-        else
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, MOE_LDS(sb + blk * 1024), 16, ob, sb_off, 0, 0);
+        if constexpr (ALAY == L_KC) load_op(KC_{}, op.a, ra, ra2, sa, b0 + i, kt, kfull, kany, false);
+        else load_op(KM_{}, op.a, ra, ra2, sa, b0 + i, kt, kfull, kany, false);
+        if constexpr (BLAY == L_KC) load_op(KC_{}, op.b, rb, rb2, sb, b0 + i, kt, kfull, kany, GATED);
+        else load_op(KM_{}, op.b, rb, rb2, sb, b0 + i, kt, kfull, kany, false);
       }
     }
   };
 
+  // ---- fragments.  MFMA operand of lane l: row/column l % 32 of the
+  // sub-tile, k values 8 (2s + l / 32) .. +7 of sub-step s (bf16; fp32: 4
+  // values 4 (2s + l / 32) .. +3).
   const int fr_row = lane & 31;
+  // KC: 16-byte reads of row fr_row
   const int fr_a = (team * 128 + fr_row) * kRowBytes;
   const int fr_b = (wq * 64 + fr_row) * kRowBytes;
+  // KM bf16: two transpose reads; lane l of 16-lane group g addresses k-row
+  // kgrp + 4t + (j >> 2), columns cb + mgrp + 4 (j & 3), j = l % 16
+  const int j16 = lane & 15, g16 = lane >> 4;
+  const int tr_row = (g16 >> 1) * 8 + (j16 >> 2);
+  const int tr_col = (g16 & 1) * 16 + 4 * (j16 & 3);
+  auto km_frag = [&](const char* st, int cb, int s) -> uint4 {
+    if constexpr (ES == 2) {
+      const int phys = (((cb >> 5) ^ (j16 >> 2)) << 5) + tr_col;   // (tr_row & 3) == j16 >> 2
+      const char* p0 = st + (16 * s + tr_row) * 512 + phys * 2;
+      const uint2 lo = read_tr(p0);
+      const uint2 hi = read_tr(p0 + 4 * 512);
+      return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    } else {
+      const int k0 = 4 * (2 * s + (lane >> 5));
+      uint32_t v[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int phys = (((cb >> 5) ^ c) << 5) + fr_row;
+        v[c] = *reinterpret_cast<const uint32_t*>(st + (k0 + c) * 1024 + phys * 4);
+      }
+      return make_uint4(v[0], v[1], v[2], v[3]);
+    }
+  };
   uint4 fa[4][2], fb[2][2];   // [sub-tile][k sub-step within the half step]
   // fragments of k sub-steps 2h and 2h+1 (one half of a K step)
   auto fread = [&](const char* sa, const char* sb, int h) {
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      const int sw = ((4 * h + 2 * s2 + (lane >> 5)) ^ swz(fr_row)) << 4;
+      const int s = 2 * h + s2;
+      const int sw = ((2 * s + (lane >> 5)) ^ swz(fr_row)) << 4;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        fa[i][s2] = *reinterpret_cast<const uint4*>(sa + fr_a + i * 32 * kRowBytes + sw);
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (ALAY == L_KC)
+          fa[i][s2] = *reinterpret_cast<const uint4*>(sa + fr_a + i * 32 * kRowBytes + sw);
+        else
+          fa[i][s2] = km_frag(sa, team * 128 + i * 32, s);
+      }
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        fb[j][s2] = *reinterpret_cast<const uint4*>(sb + fr_b + j * 32 * kRowBytes + sw);
+      for (int j = 0; j < 2; ++j) {
+        if constexpr (BLAY == L_KC)
+          fb[j][s2] = *reinterpret_cast<const uint4*>(sb + fr_b + j * 32 * kRowBytes + sw);
+        else
+          fb[j][s2] = km_frag(sb, wq * 64 + j * 32, s);
+      }
     }
   };
   auto mma = [&]() {
@@ -373,17 +468,20 @@ enum Mode {
   M_FWD1 = 0,        // H = X W1^T -> A = act(H) [, H saved]
   M_FWD1_SWIGLU = 1, // H1, H3 -> A = silu(H1) H3 [, H1 H3 saved]
   M_STORE = 2,       // plain store (Y, dX)
-  M_BWD_DA = 3,      // dA = dY W2 -> dH = dA act'(H), row-major + transposed
+  M_BWD_DA = 3,      // dA = dY W2 -> dH = dA act'(H)
   M_BWD_DA_SWIGLU = 4,
   M_DW = 5           // var-K weight gradient, fp32
 };
 
 struct GemmParams {
-  // operands (bytes)
+  // operands (bytes).  var-M: A rows of the dispatched buffer, B the
+  // expert's weights (B2: W3 of the gated forward, or the k-rows from split
+  // on of a K-major B).  var-K: A and B dispatched buffers read K-major.
   const char* A; int64_t lda;
   const char* B; const char* B2; int64_t ldb; int64_t b_gstride;
-  int64_t kbytes;     // var-M: K extent in bytes
-  int N;              // var-M: output columns;  var-K: output columns (N_out)
+  int K;              // var-M: k values
+  int kmsplit;        // var-M, K-major B: first k-row taken from B2
+  int N;              // output columns
   int M_out;          // var-K: output rows
   int ntiles;         // tiles along N
   int mtiles_out;     // var-K: tiles along M
@@ -391,7 +489,6 @@ struct GemmParams {
   // outputs
   char* C; int64_t ldc;           // row-major output (bytes per row)
   char* H1; char* H3; int64_t ldh; // saved / read pre-activations (bytes per row)
-  char* CT; int64_t ldct;          // transposed output (bytes per row)
   int f;                           // SwiGLU: width of one half
   float* dwA; float* dwB; int64_t dw_gstride; int split_row;
   float* partial; int64_t slot_elems;
@@ -417,20 +514,28 @@ __device__ __forceinline__ void decode_grouped(int L, int n_mt, int n_nt, int& m
   }
 }
 
-// PASS only names the instance (forward H, forward Y, backward dA, dX, dW2,
-// dW1/dW3), so each product is a separate kernel in traces.
+// The products: PASS names the instance (so each is its own kernel in
+// traces) and fixes the operand layouts.
 enum Pass { P_FWD_H = 0, P_FWD_Y = 1, P_BWD_DA = 2, P_BWD_DX = 3, P_BWD_DW2 = 4, P_BWD_DW13 = 5 };
+__host__ __device__ constexpr int a_layout(int pass) {
+  return pass == P_BWD_DW2 || pass == P_BWD_DW13 ? L_KM : L_KC;
+}
+__host__ __device__ constexpr int b_layout(int pass) {
+  return pass == P_FWD_H || pass == P_FWD_Y ? L_KC : L_KM;
+}
 
 template <typename T, int MODE, int PASS>
 __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams p) {
   // two stages of the A and B tiles, four distinct objects (see mainloop);
-  // after the K loop the same memory holds each wave's epilogue strips
+  // after the K loop the same memory holds each wave's epilogue strip
   __shared__ __attribute__((aligned(16))) char la0[kTileBytes];
   __shared__ __attribute__((aligned(16))) char lb0[kTileBytes];
   __shared__ __attribute__((aligned(16))) char la1[kTileBytes];
   __shared__ __attribute__((aligned(16))) char lb1[kTileBytes];
   constexpr int ES = sizeof(T);
   constexpr bool VARK = MODE == M_DW;
+  constexpr bool GATED = MODE == M_FWD1_SWIGLU;
+  constexpr int ALAY = a_layout(PASS), BLAY = b_layout(PASS);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int team = wave >> 2, wq = wave & 3;
@@ -438,7 +543,7 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
   const int n_items = VARK ? sc.n_segs * p.mtiles_out * p.ntiles : sc.n_mtiles * p.ntiles;
   const int G = gridDim.x;
   const int lbase = (blockIdx.x % kXcds) * (G / kXcds) + blockIdx.x / kXcds;
-  // the wave's two staging strips (kStripsPerArray per 32 KB array)
+  // the wave's staging strip (kStripsPerArray per 32 KB array)
   auto strip_at = [&](int sidx) {
     const int arr = sidx / kStripsPerArray, off = (sidx % kStripsPerArray) * kStripBytes;
     char* base = arr == 0 ? la0 : (arr == 1 ? lb0 : la1);
@@ -454,36 +559,34 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
     int z;
     asm volatile("s_mov_b32 %0, 0" : "=s"(z));
     float* strip = strip_at(2 * wave) + z;
-    float* strip3 = strip_at(2 * wave + 1) + z;
     TileOps op;
     int g, row0, m_valid;       // var-M: expert, first global row, valid rows in tile
     int n0;                      // first output column of the tile
-    int local_m0 = 0;            // var-M: first expert-local row
     int slot = -1, mt, nt;
-    op.b3 = nullptr;
     if constexpr (!VARK) {
       int mti;
       decode_grouped(L, sc.n_mtiles, p.ntiles, mti, nt);
       const int2 tm = p.mtile[mti];
       g = tm.x;
-      local_m0 = tm.y;
       row0 = p.offsets[g] + tm.y;
       m_valid = min(BM, sc.rows[g] - tm.y);
-      op.a = p.A + static_cast<int64_t>(row0) * p.lda;
-      op.lda = p.lda;
-      op.a_rows = m_valid;
-      op.kbytes = static_cast<int>(p.kbytes);
-      op.ldb = p.ldb;
+      op.a = {p.A + static_cast<int64_t>(row0) * p.lda, nullptr, p.lda, m_valid, 0};
+      op.K = p.K;
       const char* bg = p.B + static_cast<int64_t>(g) * p.b_gstride;
-      if constexpr (MODE == M_FWD1_SWIGLU) {
+      if constexpr (GATED) {
         n0 = nt * (BN / 2);  // hidden units covered by this tile (W1 and W3 rows)
-        op.b = bg + static_cast<int64_t>(n0) * p.ldb;
-        op.b3 = p.B2 + static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0) * p.ldb;
-        op.b_rows = min(BN / 2, p.N - n0);
-      } else {
+        op.b = {bg + static_cast<int64_t>(n0) * p.ldb,
+                p.B2 + static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0) * p.ldb,
+                p.ldb, min(BN / 2, p.N - n0), 0};
+      } else if constexpr (BLAY == L_KC) {
         n0 = nt * BN;
-        op.b = bg + static_cast<int64_t>(n0) * p.ldb;
-        op.b_rows = min(BN, p.N - n0);
+        op.b = {bg + static_cast<int64_t>(n0) * p.ldb, nullptr, p.ldb, min(BN, p.N - n0), 0};
+      } else {  // K-major weights: k-row 0, column n0
+        n0 = nt * BN;
+        op.b = {bg + static_cast<int64_t>(n0) * ES,
+                p.B2 ? p.B2 + static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0) * ES
+                     : nullptr,
+                p.ldb, min(BN, p.N - n0), p.B2 ? p.kmsplit : 0x7FFFFFFF};
       }
     } else {
       const int tmn = p.mtiles_out * p.ntiles;
@@ -492,25 +595,24 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
       const int4 sg = p.seg[si];
       g = sg.x;
       slot = sg.w;
-      const int col = sc.kbase[g] + sg.y;   // first K column of this segment
+      // this segment's dispatched rows: offsets[g] + [k0, k1) of the expert
+      const int k1 = min(sg.z, sc.rows[g]);
+      const int64_t krow = static_cast<int64_t>(p.offsets[g]) + sg.y;
       row0 = mt * BM;
       n0 = nt * BN;
       m_valid = min(BM, p.M_out - row0);
-      op.a = p.A + static_cast<int64_t>(row0) * p.lda + static_cast<int64_t>(col) * ES;
-      op.lda = p.lda;
-      op.a_rows = m_valid;
-      op.ldb = p.ldb;
-      op.b = p.B + static_cast<int64_t>(n0) * p.ldb + static_cast<int64_t>(col) * ES;
-      op.b_rows = min(BN, p.N - n0);
-      op.kbytes = (sg.z - sg.y) * ES;
+      op.a = {p.A + krow * p.lda + static_cast<int64_t>(row0) * ES, nullptr, p.lda, m_valid,
+              0x7FFFFFFF};
+      op.b = {p.B + krow * p.ldb + static_cast<int64_t>(n0) * ES, nullptr, p.ldb,
+              min(BN, p.N - n0), 0x7FFFFFFF};
+      op.K = max(0, k1 - sg.y);
     }
 
     floatx16 acc[4][2];
-    constexpr bool GATED = MODE == M_FWD1_SWIGLU;
-    if (op.a_rows >= BM && op.b_rows >= (GATED ? BN / 2 : BN) && op.kbytes % kRowBytes == 0)
-      mainloop<T, GATED, true>(op, la0, lb0, la1, lb1, acc);
+    if (op.a.rows >= BM && op.b.rows >= (GATED ? BN / 2 : BN))
+      mainloop<T, ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc);
     else
-      mainloop<T, GATED, false>(op, la0, lb0, la1, lb1, acc);
+      mainloop<T, ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc);
 
     // Epilogue, wave by wave: 16 accumulator rows at a time go through the
     // wave's own LDS strip, then each lane finishes 8 consecutive columns of
@@ -572,60 +674,27 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
             const int r = it * 8 + (lane >> 3), c8 = (lane & 7) * 8;
             const int lm = srow0 + r;
             const int gc = n0 + wcol + c8;
-            float g1[8], g3[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) g1[e] = g3[e] = 0.f;
             if (lm < m_valid && gc < p.N) {
               const int64_t grow = row0 + lm;
-              float h1[8];
+              float h1[8], g1[8];
               load_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h1);
               if constexpr (SW) {
-                float h3[8];
+                float h3[8], g3[8];
                 load_vec<T>(p.H3 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h3);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                   const float da = strip[r * kStripPitch + c8 + e];
                   const float sg = sigm(h1[e]);
-                  g1[e] = Elem<T>::to_f(Elem<T>::from_f(da * h3[e] * sg * (1.f + h1[e] * (1.f - sg))));
-                  g3[e] = Elem<T>::to_f(Elem<T>::from_f(da * h1[e] * sg));
+                  g1[e] = da * h3[e] * sg * (1.f + h1[e] * (1.f - sg));
+                  g3[e] = da * h1[e] * sg;
                 }
                 store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
                 store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(p.f + gc) * ES, g3);
               } else {
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                  g1[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kStripPitch + c8 + e] *
-                                                         act_grad_f(h1[e], p.act)));
+                  g1[e] = strip[r * kStripPitch + c8 + e] * act_grad_f(h1[e], p.act);
                 store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
-              }
-            }
-            // keep the rounded gradients for the transposed store (in place:
-            // each lane rewrites exactly the elements it read); rows past the
-            // expert's rows become zero (the transposed buffers are zero-padded)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              strip[r * kStripPitch + c8 + e] = g1[e];
-              if constexpr (SW) strip3[r * kStripPitch + c8 + e] = g3[e];
-            }
-          }
-          // transposed store: 8 consecutive expert rows of one column per lane
-          const int kcol0 = sc.kbase[g] + local_m0 + srow0;   // first transposed column
-          const int kpad_g = (sc.rows[g] + kTT - 1) / kTT * kTT;
-          const int gc = n0 + wcol + lane;
-#pragma unroll
-          for (int it = 0; it < 2; ++it) {
-            const int rg = it * 8;
-            if (gc < p.N && local_m0 + srow0 + rg < kpad_g) {
-              float v[8];
-#pragma unroll
-              for (int e = 0; e < 8; ++e) v[e] = strip[(rg + e) * kStripPitch + lane];
-              store_vec<T>(p.CT + static_cast<int64_t>(gc) * p.ldct +
-                               static_cast<int64_t>(kcol0 + rg) * ES, v);
-              if constexpr (SW) {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] = strip3[(rg + e) * kStripPitch + lane];
-                store_vec<T>(p.CT + static_cast<int64_t>(p.f + gc) * p.ldct +
-                                 static_cast<int64_t>(kcol0 + rg) * ES, v);
               }
             }
           }
@@ -661,88 +730,8 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
 }
 
 // ---------------------------------------------------------------------------
-// transposes
+// split-K reduction
 // ---------------------------------------------------------------------------
-enum TMode { T_COPY = 0, T_ACT = 1, T_SWIGLU = 2 };
-
-// out[c, kbase[g] + r] = op(in[offsets[g] + r, c]) for the 64-row tile list,
-// rows past the expert's rows (up to the 64 padding) written as zero.
-template <typename T, int TM>
-__global__ __launch_bounds__(256) void rows_transpose_kernel(
-    const char* __restrict__ in, const char* __restrict__ in3, int64_t ld_in, int D,
-    int act, const int32_t* __restrict__ offsets, const Sched* __restrict__ sc,
-    const int2* __restrict__ ttile, char* __restrict__ out, int64_t ld_out) {
-  constexpr int ES = sizeof(T);
-  constexpr int V = 16 / ES;          // elements per 16-byte chunk
-  constexpr int CPR = kTT / V;        // chunks per 64-element row
-  __shared__ float tile[kTT][kTT + 1];
-  if (static_cast<int>(blockIdx.x) >= sc->n_ttiles) return;
-  const int2 tt = ttile[blockIdx.x];
-  const int g = tt.x, r0 = tt.y;
-  const int c0 = blockIdx.y * kTT;
-  const int rows_g = sc->rows[g];
-  const int64_t grow0 = static_cast<int64_t>(offsets[g]) + r0;
-  for (int ch = threadIdx.x; ch < kTT * CPR; ch += 256) {
-    const int rr = ch / CPR, cc = ch % CPR;
-    const int col = c0 + cc * V;
-    float v[V];
-    if (r0 + rr < rows_g && col < D) {
-      const int64_t o = (grow0 + rr) * ld_in + static_cast<int64_t>(col) * ES;
-      const uint4 raw = *reinterpret_cast<const uint4*>(in + o);
-      Elem<T>::load(raw, v);
-      if constexpr (TM == T_ACT) {
-#pragma unroll
-        for (int e = 0; e < V; ++e) v[e] = act_f(v[e], act);
-      } else if constexpr (TM == T_SWIGLU) {
-        float h3[V];
-        Elem<T>::load(*reinterpret_cast<const uint4*>(in3 + o), h3);
-#pragma unroll
-        for (int e = 0; e < V; ++e) v[e] = v[e] * sigm(v[e]) * h3[e];
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < V; ++e) v[e] = 0.f;
-    }
-#pragma unroll
-    for (int e = 0; e < V; ++e) tile[rr][cc * V + e] = v[e];
-  }
-  __syncthreads();
-  const int64_t kcol = static_cast<int64_t>(sc->kbase[g]) + r0;
-  for (int ch = threadIdx.x; ch < kTT * CPR; ch += 256) {
-    const int oc = ch / CPR, rc = ch % CPR;
-    if (c0 + oc >= D) continue;
-    float v[V];
-#pragma unroll
-    for (int e = 0; e < V; ++e) v[e] = tile[rc * V + e][oc];
-    *reinterpret_cast<uint4*>(out + static_cast<int64_t>(c0 + oc) * ld_out +
-                              (kcol + rc * V) * ES) = Elem<T>::store(v);
-  }
-}
-
-// out[g, c, co + r] = in[g, r, c] for in [E, R, C] (weights), for the experts
-// that have rows (the others' transposed weights are never read).
-template <typename T>
-__global__ __launch_bounds__(256) void weight_transpose_kernel(
-    const T* __restrict__ in, int R, int C, T* __restrict__ out, int64_t ld_out, int co,
-    int64_t out_gstride, const Sched* __restrict__ sc) {
-  __shared__ T tile[kTT][kTT + 1];
-  const int g = blockIdx.z;
-  if (sc->rows[g] == 0) return;
-  const int c0 = blockIdx.x * kTT, r0 = blockIdx.y * kTT;
-  const T* src = in + static_cast<int64_t>(g) * R * C;
-  T* dst = out + static_cast<int64_t>(g) * out_gstride;
-  for (int i = threadIdx.x; i < kTT * kTT; i += 256) {
-    const int rr = i / kTT, cc = i % kTT;
-    if (r0 + rr < R && c0 + cc < C) tile[rr][cc] = src[static_cast<int64_t>(r0 + rr) * C + c0 + cc];
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < kTT * kTT; i += 256) {
-    const int cc = i / kTT, rr = i % kTT;
-    if (r0 + rr < R && c0 + cc < C)
-      dst[static_cast<int64_t>(c0 + cc) * ld_out + co + r0 + rr] = tile[rr][cc];
-  }
-}
-
 // dW[g] = sum over the expert's split slots, in slot order.
 __global__ __launch_bounds__(256) void split_reduce_kernel(
     const float* __restrict__ partial, int64_t slot_elems, const Sched* __restrict__ sc,
@@ -794,11 +783,11 @@ struct FfnPlan {
   int E, d, f, F;            // F = f (relu/gelu) or 2f (swiglu)
   int64_t rows_alloc;
   size_t es;
-  int max_mtiles, max_ttiles, kpad_cap, max_segs, max_slots, tmn_min;
+  int max_mtiles, max_segs, max_slots, tmn_min;
   int64_t slot_elems;
   // byte offsets inside the workspace
-  size_t o_sched, o_mtile, o_ttile, o_seg, o_end_sched;
-  size_t o_abuf, o_w2t, o_w13t, o_dh, o_dht, o_xt, o_dyt, o_at, o_part, total_fwd, total_bwd;
+  size_t o_sched, o_mtile, o_seg, o_end_sched;
+  size_t o_abuf, o_dh, o_part, total_fwd, total_bwd;
 };
 
 bool make_plan(moe_dtype dt, moe_act act, int E, int d, int f, int64_t rows_alloc, FfnPlan& pl) {
@@ -808,44 +797,34 @@ bool make_plan(moe_dtype dt, moe_act act, int E, int d, int f, int64_t rows_allo
   pl.E = E; pl.d = d; pl.f = f; pl.F = act == MOE_SWIGLU ? 2 * f : f;
   pl.rows_alloc = rows_alloc;
   pl.es = esize(dt);
+  // every operand offset inside a 256-row tile (K-contiguous operands) or a
+  // K step (K-major ones) stays below 2^31 bytes: buffer loads take 32-bit
+  // offsets
+  const int64_t max_ld = static_cast<int64_t>(pl.es) * (2 * static_cast<int64_t>(f) > d ? 2 * static_cast<int64_t>(f) : d);
+  if (max_ld > kMaxOperandRowBytes) return false;
   pl.max_mtiles = cdiv(rows_alloc, BM) + E;
-  pl.max_ttiles = cdiv(rows_alloc, kTT) + E;
-  const int64_t kcap = (rows_alloc + kTT - 1) / kTT * kTT + static_cast<int64_t>(kTT) * E;
-  // every GEMM operand offset inside a 256-row tile stays below 2^31 bytes
-  // (buffer-resource loads with 32-bit offsets)
-  int64_t max_ld = kcap;
-  if (2 * static_cast<int64_t>(f) > max_ld) max_ld = 2 * static_cast<int64_t>(f);
-  if (d > max_ld) max_ld = d;
-  if (max_ld * static_cast<int64_t>(pl.es) > kMaxOperandRowBytes) return false;
-  pl.kpad_cap = static_cast<int>(kcap);
   const int tmn2 = cdiv(d, BM) * cdiv(f, BN);
   const int tmn13 = cdiv(pl.F, BM) * cdiv(d, BN);
   pl.tmn_min = tmn2 < tmn13 ? tmn2 : tmn13;
-  int slots_a = 1024 / pl.tmn_min;
-  int slots_b = static_cast<int>(2 * kcap / kSplitFloor);
-  pl.max_slots = (slots_a < slots_b ? slots_a : slots_b) + 1;
+  const int64_t kcap = (rows_alloc + kKc - 1) / kKc * kKc + static_cast<int64_t>(kKc) * E;
+  const int64_t slots_a = 1024 / pl.tmn_min;
+  const int64_t slots_b = 2 * kcap / kSplitFloor;
+  pl.max_slots = static_cast<int>(slots_a < slots_b ? slots_a : slots_b) + 1;
   pl.max_segs = E + pl.max_slots;
   pl.slot_elems = static_cast<int64_t>(pl.F) * d > static_cast<int64_t>(d) * f
                       ? static_cast<int64_t>(pl.F) * d : static_cast<int64_t>(d) * f;
   size_t o = 0;
   pl.o_sched = o; o = align_up(o + sizeof(Sched), 256);
   pl.o_mtile = o; o = align_up(o + sizeof(int2) * pl.max_mtiles, 256);
-  pl.o_ttile = o; o = align_up(o + sizeof(int2) * pl.max_ttiles, 256);
   pl.o_seg = o;   o = align_up(o + sizeof(int4) * pl.max_segs, 256);
   pl.o_end_sched = o;
   const size_t es = pl.es;
-  // forward: the activation buffer A [rows_alloc, f]
+  // forward: the activation buffer A [rows_alloc, f] when no h_save is given
   pl.o_abuf = o;
   pl.total_fwd = align_up(o + static_cast<size_t>(rows_alloc) * f * es, 256);
-  // backward
+  // backward: dH [rows_alloc, F] and the split partial sums
   o = pl.o_end_sched;
-  pl.o_w2t = o;  o = align_up(o + static_cast<size_t>(E) * f * d * es, 256);
-  pl.o_w13t = o; o = align_up(o + static_cast<size_t>(E) * d * pl.F * es, 256);
   pl.o_dh = o;   o = align_up(o + static_cast<size_t>(rows_alloc) * pl.F * es, 256);
-  pl.o_dht = o;  o = align_up(o + static_cast<size_t>(pl.F) * kcap * es, 256);
-  pl.o_xt = o;   o = align_up(o + static_cast<size_t>(d) * kcap * es, 256);
-  pl.o_dyt = o;  o = align_up(o + static_cast<size_t>(d) * kcap * es, 256);
-  pl.o_at = o;   o = align_up(o + static_cast<size_t>(f) * kcap * es, 256);
   pl.o_part = o; o = align_up(o + static_cast<size_t>(pl.max_slots) * pl.slot_elems * 4, 256);
   pl.total_bwd = o;
   return true;
@@ -855,9 +834,8 @@ moe_status launch_schedule(hipStream_t s, const FfnPlan& pl, const int32_t* offs
                            const int32_t* rows, char* ws) {
   MOE_TIMED("ffn_schedule", s);
   schedule_kernel<<<1, 64, 0, s>>>(
-      offsets, rows, pl.E, pl.rows_alloc, pl.max_mtiles, pl.max_ttiles, pl.kpad_cap,
-      pl.max_segs, pl.tmn_min, pl.max_slots, reinterpret_cast<Sched*>(ws + pl.o_sched),
-      reinterpret_cast<int2*>(ws + pl.o_mtile), reinterpret_cast<int2*>(ws + pl.o_ttile),
+      offsets, rows, pl.E, pl.rows_alloc, pl.max_mtiles, pl.max_segs, pl.tmn_min, pl.max_slots,
+      reinterpret_cast<Sched*>(ws + pl.o_sched), reinterpret_cast<int2*>(ws + pl.o_mtile),
       reinterpret_cast<int4*>(ws + pl.o_seg));
   MOE_LAUNCH_CHECK();
   return MOE_OK;
@@ -869,6 +847,7 @@ GemmParams base_params(const FfnPlan& pl, const int32_t* offsets, char* ws) {
   p.sched = reinterpret_cast<const Sched*>(ws + pl.o_sched);
   p.mtile = reinterpret_cast<const int2*>(ws + pl.o_mtile);
   p.seg = reinterpret_cast<const int4*>(ws + pl.o_seg);
+  p.kmsplit = 0x7FFFFFFF;
   return p;
 }
 
@@ -895,46 +874,6 @@ moe_status launch_gemm(hipStream_t s, moe_dtype dt, const GemmParams& p) {
     moe_status st_ = (__VA_ARGS__);        \
     if (st_ != MOE_OK) return st_;         \
   } while (0)
-
-template <int TM>
-moe_status launch_rows_transpose(hipStream_t s, moe_dtype dt, const FfnPlan& pl,
-                                 const int32_t* offsets, char* ws, const void* in,
-                                 const void* in3, int D, int act, char* out) {
-  dim3 grid(pl.max_ttiles, cdiv(D, kTT));
-  const Sched* sc = reinterpret_cast<const Sched*>(ws + pl.o_sched);
-  const int2* tt = reinterpret_cast<const int2*>(ws + pl.o_ttile);
-  const int64_t ld_in = static_cast<int64_t>(D) * pl.es;
-  const int64_t ld_out = static_cast<int64_t>(pl.kpad_cap) * pl.es;
-  MOE_TIMED("transpose_rows", s);
-  if (dt == MOE_BF16)
-    rows_transpose_kernel<uint16_t, TM><<<grid, 256, 0, s>>>(
-        static_cast<const char*>(in), static_cast<const char*>(in3), ld_in, D, act, offsets, sc,
-        tt, out, ld_out);
-  else
-    rows_transpose_kernel<float, TM><<<grid, 256, 0, s>>>(
-        static_cast<const char*>(in), static_cast<const char*>(in3), ld_in, D, act, offsets, sc,
-        tt, out, ld_out);
-  MOE_LAUNCH_CHECK();
-  return MOE_OK;
-}
-
-moe_status launch_weight_transpose(hipStream_t s, moe_dtype dt, const FfnPlan& pl, char* ws,
-                                   const void* in, int E, int R, int C, char* out,
-                                   int64_t ld_out, int co, int64_t gstride) {
-  dim3 grid(cdiv(C, kTT), cdiv(R, kTT), E);
-  const Sched* sc = reinterpret_cast<const Sched*>(ws + pl.o_sched);
-  MOE_TIMED("transpose_weights", s);
-  if (dt == MOE_BF16)
-    weight_transpose_kernel<uint16_t><<<grid, 256, 0, s>>>(
-        static_cast<const uint16_t*>(in), R, C, reinterpret_cast<uint16_t*>(out), ld_out, co,
-        gstride, sc);
-  else
-    weight_transpose_kernel<float><<<grid, 256, 0, s>>>(
-        static_cast<const float*>(in), R, C, reinterpret_cast<float*>(out), ld_out, co, gstride,
-        sc);
-  MOE_LAUNCH_CHECK();
-  return MOE_OK;
-}
 
 moe_status launch_split_reduce(hipStream_t s, const FfnPlan& pl, char* ws, int M_out, int N,
                                float* dwA, float* dwB, int split_row) {
@@ -986,7 +925,10 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   char* ws = static_cast<char*>(workspace);
   MOE_TRY(launch_schedule(s, pl, offsets, rows, ws));
   const int64_t es = static_cast<int64_t>(pl.es);
-  char* abuf = ws + pl.o_abuf;
+  const int64_t plane = rows_alloc * f * es;   // one [rows_alloc, f] plane of h_save
+  const bool sw = act == MOE_SWIGLU;
+  // A = act(H): the last plane of h_save when the caller keeps activations
+  char* abuf = h_save ? static_cast<char*>(h_save) + (sw ? 2 : 1) * plane : ws + pl.o_abuf;
 
   GemmParams p = base_params(pl, offsets, ws);
   p.A = static_cast<const char*>(x_disp);
@@ -995,16 +937,16 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   p.B2 = static_cast<const char*>(w3);
   p.ldb = d * es;
   p.b_gstride = static_cast<int64_t>(f) * d * es;
-  p.kbytes = d * es;
+  p.K = d;
   p.N = f;
   p.act = act == MOE_RELU ? ACT_RELU : (act == MOE_GELU_TANH ? ACT_GELU : ACT_SWIGLU);
   p.C = abuf;
   p.ldc = f * es;
   p.H1 = static_cast<char*>(h_save);
-  p.H3 = h_save ? static_cast<char*>(h_save) + rows_alloc * f * es : nullptr;
+  p.H3 = h_save ? static_cast<char*>(h_save) + plane : nullptr;
   p.ldh = f * es;
-  if (act == MOE_SWIGLU) {
-    p.ntiles = cdiv(f, 128);
+  if (sw) {
+    p.ntiles = cdiv(f, BN / 2);
     MOE_TRY(launch_gemm<M_FWD1_SWIGLU, P_FWD_H>(s, dt, p));
   } else {
     p.ntiles = cdiv(f, BN);
@@ -1017,7 +959,7 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   q.B = static_cast<const char*>(w2);
   q.ldb = f * es;
   q.b_gstride = static_cast<int64_t>(d) * f * es;
-  q.kbytes = f * es;
+  q.K = f;
   q.N = d;
   q.ntiles = cdiv(d, BN);
   q.C = static_cast<char*>(y_disp);
@@ -1050,34 +992,21 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   const int64_t es = static_cast<int64_t>(pl.es);
   const bool sw = act == MOE_SWIGLU;
   const int F = pl.F;
-  char* w2t = ws + pl.o_w2t;    // [E, f, d]
-  char* w13t = ws + pl.o_w13t;  // [E, d, F]
-  char* dh = ws + pl.o_dh;      // [rows_alloc, F]
-  char* dht = ws + pl.o_dht;    // [F, kpad_cap]
-  char* xt = ws + pl.o_xt;      // [d, kpad_cap]
-  char* dyt = ws + pl.o_dyt;    // [d, kpad_cap]
-  char* at = ws + pl.o_at;      // [f, kpad_cap]
+  char* dh = ws + pl.o_dh;      // [rows_alloc, F]: dH, or [dH1 | dH3]
   const int actc = act == MOE_RELU ? ACT_RELU : (act == MOE_GELU_TANH ? ACT_GELU : ACT_SWIGLU);
+  const int64_t plane = rows_alloc * f * es;
   const char* h1 = static_cast<const char*>(h_save);
-  const char* h3 = sw ? h1 + rows_alloc * f * es : nullptr;
+  const char* h3 = sw ? h1 + plane : nullptr;
+  const char* abuf = h1 + (sw ? 2 : 1) * plane;   // A = act(H), saved by the forward
 
-  // weights to K-contiguous form for the data-gradient products
-  MOE_TRY(launch_weight_transpose(s, dt, pl, ws, w2, E, d, f, w2t, d, 0,
-                                  static_cast<int64_t>(f) * d));
-  MOE_TRY(launch_weight_transpose(s, dt, pl, ws, w1, E, f, d, w13t, F, 0,
-                                  static_cast<int64_t>(d) * F));
-  if (sw)
-    MOE_TRY(launch_weight_transpose(s, dt, pl, ws, w3, E, f, d, w13t, F, f,
-                                    static_cast<int64_t>(d) * F));
-
-  // dA = dY W2 -> dH (row-major and transposed)
+  // dA = dY W2 (W2 read K-major: its rows are the d inputs) -> dH
   GemmParams p = base_params(pl, offsets, ws);
   p.A = static_cast<const char*>(dy_disp);
   p.lda = d * es;
-  p.B = w2t;
-  p.ldb = d * es;
-  p.b_gstride = static_cast<int64_t>(f) * d * es;
-  p.kbytes = d * es;
+  p.B = static_cast<const char*>(w2);
+  p.ldb = f * es;
+  p.b_gstride = static_cast<int64_t>(d) * f * es;
+  p.K = d;
   p.N = f;
   p.ntiles = cdiv(f, BN);
   p.act = actc;
@@ -1086,42 +1015,34 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   p.H1 = const_cast<char*>(h1);
   p.H3 = const_cast<char*>(h3);
   p.ldh = f * es;
-  p.CT = dht;
-  p.ldct = static_cast<int64_t>(pl.kpad_cap) * es;
   p.f = f;
   if (sw) MOE_TRY(launch_gemm<M_BWD_DA_SWIGLU, P_BWD_DA>(s, dt, p));
   else MOE_TRY(launch_gemm<M_BWD_DA, P_BWD_DA>(s, dt, p));
 
-  // dx_disp = [dH1 | dH3] [W1 | W3]
+  // dx_disp = [dH1 | dH3] [W1; W3] (W1, W3 read K-major, W3 from k = f on)
   GemmParams q = base_params(pl, offsets, ws);
   q.A = dh;
   q.lda = F * es;
-  q.B = w13t;
-  q.ldb = F * es;
-  q.b_gstride = static_cast<int64_t>(d) * F * es;
-  q.kbytes = F * es;
+  q.B = static_cast<const char*>(w1);
+  q.B2 = sw ? static_cast<const char*>(w3) : nullptr;
+  q.kmsplit = sw ? f : 0x7FFFFFFF;
+  q.ldb = d * es;
+  q.b_gstride = static_cast<int64_t>(f) * d * es;
+  q.K = F;
   q.N = d;
   q.ntiles = cdiv(d, BN);
   q.C = static_cast<char*>(dx_disp);
   q.ldc = d * es;
   MOE_TRY(launch_gemm<M_STORE, P_BWD_DX>(s, dt, q));
 
-  // K-contiguous copies of the row operands of the weight gradients
-  MOE_TRY(launch_rows_transpose<T_COPY>(s, dt, pl, offsets, ws, x_disp, nullptr, d, 0, xt));
-  MOE_TRY(launch_rows_transpose<T_COPY>(s, dt, pl, offsets, ws, dy_disp, nullptr, d, 0, dyt));
-  if (sw)
-    MOE_TRY(launch_rows_transpose<T_SWIGLU>(s, dt, pl, offsets, ws, h1, h3, f, actc, at));
-  else
-    MOE_TRY(launch_rows_transpose<T_ACT>(s, dt, pl, offsets, ws, h1, nullptr, f, actc, at));
-
-  // dW2 [d, f] = dY^T A
+  // dW2 [d, f] = dY^T A, contracting over each expert's dispatched rows
   GemmParams r = base_params(pl, offsets, ws);
-  r.A = dyt;
-  r.lda = static_cast<int64_t>(pl.kpad_cap) * es;
+  r.A = static_cast<const char*>(dy_disp);
+  r.lda = d * es;
   r.M_out = d;
   r.mtiles_out = cdiv(d, BM);
-  r.B = at;
-  r.ldb = static_cast<int64_t>(pl.kpad_cap) * es;
+  r.B = abuf;
+  r.ldb = f * es;
   r.N = f;
   r.ntiles = cdiv(f, BN);
   r.dwA = dw2;
@@ -1135,12 +1056,12 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
 
   // [dW1; dW3] [F, d] = [dH1 dH3]^T X
   GemmParams u = base_params(pl, offsets, ws);
-  u.A = dht;
-  u.lda = static_cast<int64_t>(pl.kpad_cap) * es;
+  u.A = dh;
+  u.lda = F * es;
   u.M_out = F;
   u.mtiles_out = cdiv(F, BM);
-  u.B = xt;
-  u.ldb = static_cast<int64_t>(pl.kpad_cap) * es;
+  u.B = static_cast<const char*>(x_disp);
+  u.ldb = d * es;
   u.N = d;
   u.ntiles = cdiv(d, BN);
   u.dwA = dw1;

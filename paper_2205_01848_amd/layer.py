@@ -64,7 +64,8 @@ class MoELayer:
         self.backward_enabled = backward
         self.h_save = None
         if backward:
-            self.h_save = e((2 if self.swiglu else 1) * max(R, 1) * f)
+            # H (or H1, H3) and A = act(H), kept for the backward
+            self.h_save = e((3 if self.swiglu else 2) * max(R, 1) * f)
             self.dy_disp = e(max(R, 1), d)
             self.dx_disp = e(max(R, 1), d)
             self.dweights = e(T, k, t=f32)

@@ -69,7 +69,7 @@ def _gpu(rows, cap, off, R, P, act, dt, E, d, f, rows_kind="fill"):
     code = B.MOE_BF16 if dt == "bf16" else B.MOE_F32
     x, w1, w2, dy = (to_dev(P[n], dt) for n in ("x", "w1", "w2", "dy"))
     w3 = to_dev(P["w3"], dt) if P["w3"] is not None else None
-    n_h = 2 if act == "swiglu" else 1
+    n_h = 3 if act == "swiglu" else 2   # H (or H1, H3), then A = act(H)
     h = torch.full((n_h * R * f,), float("nan"), dtype=td, device=dev())
     y = torch.full((R, d), float("nan"), dtype=td, device=dev())
     ws = B.workspace(B.moe_ffn_fwd_workspace_bytes(code, a, E, d, f, R), dev())
@@ -92,6 +92,7 @@ def _compare(g, valid, fw, bw, act, dt, exact):
     cmp(g["h"][0][valid], fw["H"], "H")
     if act == "swiglu":
         cmp(g["h"][1][valid], fw["H3"], "H3")
+    cmp(g["h"][-1][valid], fw["A"], "A")
     cmp(g["y"][valid], fw["Y"], "Y")
     cmp(g["dx"][valid], bw["dX"], "dX")
     cmp(g["dw1"], bw["dW1"], "dW1")

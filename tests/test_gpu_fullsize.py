@@ -140,12 +140,13 @@ def _check(name, run):
         assert (to_np(L.y)[dropped[:4]] == 0).all()
     if not wl.backward:
         return
-    hs = L.h_save.view(-1, R, wl.f) if L.swiglu else L.h_save.view(R, wl.f)
+    hs = L.h_save.view(-1, R, wl.f)   # H (or H1, H3), then A = act(H)
     if L.swiglu:
         assert_close(_rows(hs[0], dt, rows), fr["H"], rt, "H1 rows")
         assert_close(_rows(hs[1], dt, rows), fr["H3"], rt, "H3 rows")
     else:
-        assert_close(_rows(hs, dt, rows), fr["H"], rt, "H rows")
+        assert_close(_rows(hs[0], dt, rows), fr["H"], rt, "H rows")
+    assert_close(_rows(hs[-1], dt, rows), fr["A"], rt, "A rows")
 
     # ---- backward on the sampled tokens ----------------------------------------------
     dY = O.as_f64(I.dy, dt)
