@@ -8,4 +8,8 @@ passage of the paper (Kossmann, Jia, Aiken, "Optimizing Mixture of Experts
 using Dynamic Recompilations", MLSys 2022) that it follows.
 """
 from .moe_oracle import *  # noqa: F401,F403
-from .moe_oracle import __all__  # noqa: F401
+from .losses import *  # noqa: F401,F403
+from .policies import *  # noqa: F401,F403
+from . import losses as _losses, moe_oracle as _core, policies as _policies
+
+__all__ = list(_core.__all__) + list(_losses.__all__) + list(_policies.__all__)

@@ -480,13 +480,16 @@ def combine_bwd(dy: np.ndarray, Y_disp: np.ndarray, dest_row: np.ndarray,
 # gate backward and dispatch backward
 # ----------------------------------------------------------------------------
 def gate_bwd(logits: np.ndarray, ids: np.ndarray, dweights: np.ndarray,
-             renorm: int, x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+             renorm: int, x: np.ndarray,
+             dprob_coef: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
     """Gradient through normalize(score[indices]) and the softmax to the gate
     logits, then to the gate weights.
 
     raw:    g_j = dw_j
     renorm: w_j = p_j / S with S = sum_j p_j, so g_j = (dw_j - sum_i dw_i w_i) / S
-    dp[t,e] = sum_j [ids[t,j] = e] g_j;  dl = p * (dp - <dp, p>);
+    dp[t,e] = sum_j [ids[t,j] = e] g_j (+ dprob_coef[e], a gradient that is
+    the same for every token, such as Eq. 3's balance term);
+    dl = p * (dp - <dp, p>);
     dW_g[e,i] = sum_t dl[t,e] x[t,i].  dl and dW_g are float32."""
     p = softmax(logits)
     T, E = p.shape
@@ -502,6 +505,8 @@ def gate_bwd(logits: np.ndarray, ids: np.ndarray, dweights: np.ndarray,
     dp = np.zeros((T, E))
     for j in range(idx.shape[1]):
         dp[np.arange(T), idx[:, j]] += g[:, j]
+    if dprob_coef is not None:
+        dp += np.asarray(dprob_coef, dtype=np.float64)[None, :]
     dl = p * (dp - (dp * p).sum(axis=1, keepdims=True))
     dl32 = _f32(dl).astype(np.float64)
     dwg = _f32(dl32.T @ x).astype(np.float64)
@@ -562,9 +567,19 @@ def layer_forward(x, w1, w3, w2, act, dtype, ids, weights, capacity,
 
 
 def layer_backward(fw, x, dy, w1, w3, w2, act, dtype, ids, weights, E,
-                   logits=None, renorm=0, w_g=None) -> Dict[str, np.ndarray]:
-    """combine_bwd -> FFN backward -> gate backward -> dispatch backward."""
-    dw, dy_disp = combine_bwd(dy, fw["Y"], fw["dest_row"], weights, dtype)
+                   logits=None, renorm=0, w_g=None, target=None,
+                   dprob_coef=None) -> Dict[str, np.ndarray]:
+    """combine_bwd -> FFN backward -> gate backward -> dispatch backward.
+
+    With `target`, the specification loss of Eq. 2 (squared error) takes the
+    place of combine_bwd and `dy` is not used; `dprob_coef` adds a dprobs
+    term shared by every token (Eq. 3's balance term) to the gate backward."""
+    spec = None
+    if target is not None:
+        from .losses import spec_loss
+        spec, dw, dy_disp = spec_loss(fw["Y"], fw["dest_row"], weights, target, dtype)
+    else:
+        dw, dy_disp = combine_bwd(dy, fw["Y"], fw["dest_row"], weights, dtype)
     rows, e_of = fw["rows"], fw["e_of"]
     d = x.shape[1]
     dx_disp = np.full((fw["x_disp"].shape[0], d), np.nan)
@@ -581,7 +596,7 @@ def layer_backward(fw, x, dy, w1, w3, w2, act, dtype, ids, weights, E,
         dW3 = np.zeros((E, f, d), dtype=np.float32) if act == "swiglu" else None
     dl = dwg = None
     if logits is not None:
-        dl, dwg = gate_bwd(logits, ids, dw, renorm, x)
+        dl, dwg = gate_bwd(logits, ids, dw, renorm, x, dprob_coef)
     dx = dispatch_bwd(dx_disp, fw["dest_row"], dl, w_g, dtype)
     return dict(dweights=dw, dy_disp=dy_disp, dx_disp=dx_disp, dW1=dW1,
-                dW2=dW2, dW3=dW3, dlogits=dl, dw_g=dwg, dx=dx)
+                dW2=dW2, dW3=dW3, dlogits=dl, dw_g=dwg, dx=dx, spec_loss=spec)

@@ -28,12 +28,14 @@ import numpy as np
 
 __all__ = [
     "Workload", "Inputs", "CONFIGS", "config", "make_inputs", "small",
-    "to_bf16_bits", "TENSOR_IDS",
+    "to_bf16_bits", "TENSOR_IDS", "make_target", "drifting_assignments",
+    "reassign_some",
 ]
 
 # tensor ids used as SeedSequence spawn keys (fixed; never renumber)
 TENSOR_IDS = {"x": 1, "w_g": 2, "bias": 3, "w1": 4, "w3": 5, "w2": 6,
-              "dy": 7, "ids": 8, "cw": 9}
+              "dy": 7, "ids": 8, "cw": 9, "target": 10, "traj": 11,
+              "reassign": 12}
 
 _CHUNK = 1 << 22  # elements per independent PCG64 stream
 
@@ -167,13 +169,10 @@ def _bias(wl: Workload) -> Optional[np.ndarray]:
     raise ValueError(wl.bias)
 
 
-def _cached_assignments(wl: Workload):
-    """Cached [T,k] ids from P(e) ~ (e+1)^-s with distinct picks per token,
-    and [T,k] weights uniform on [0,1) renormalised per token."""
-    T, E, k = wl.T, wl.E, wl.k
-    p = (np.arange(1, E + 1, dtype=np.float64)) ** (-wl.zipf_s)
-    p /= p.sum()
-    rng = _rng(wl.seed, "ids", 0)
+def _sample_distinct(rng: np.random.Generator, p: np.ndarray, T: int, k: int) -> np.ndarray:
+    """[T,k] expert ids, k distinct per token, drawn one after another from
+    p (renormalised over the experts not yet taken)."""
+    E = len(p)
     u = rng.random((T, k))
     ids = np.empty((T, k), dtype=np.int32)
     taken = np.zeros((T, E), dtype=bool)
@@ -190,6 +189,16 @@ def _cached_assignments(wl: Workload):
                 pick[t] = int(np.nonzero(~taken[t])[0][-1])
         ids[:, j] = pick
         taken[np.arange(T), pick] = True
+    return ids
+
+
+def _cached_assignments(wl: Workload):
+    """Cached [T,k] ids from P(e) ~ (e+1)^-s with distinct picks per token,
+    and [T,k] weights uniform on [0,1) renormalised per token."""
+    T, E, k = wl.T, wl.E, wl.k
+    p = (np.arange(1, E + 1, dtype=np.float64)) ** (-wl.zipf_s)
+    p /= p.sum()
+    ids = _sample_distinct(_rng(wl.seed, "ids", 0), p, T, k)
     uw = _rng(wl.seed, "cw", 0).random((T, k))
     s = uw.sum(axis=1, keepdims=True)
     w = np.where(s > 0, uw / np.where(s > 0, s, 1.0), 1.0 / k).astype(np.float32)
@@ -214,3 +223,47 @@ def make_inputs(wl: Workload) -> Inputs:
     if wl.gate == "cached":
         ids, cw = _cached_assignments(wl)
     return Inputs(wl, x, w_g, bias, w1, w3, w2, dy, ids, cw)
+
+
+def make_target(wl: Workload) -> np.ndarray:
+    """A [T,d] regression target in the layer dtype, N(0,1) entries: the
+    synthetic label of a squared-error task loss."""
+    return _normal(wl.seed, "target", (wl.T, wl.d), 1.0, wl.dtype)
+
+
+def drifting_assignments(seed: int, T: int, E: int, k: int, n_iter: int,
+                         s_start: float = 1.2, s_end: float = 0.6,
+                         swap_every: int = 5):
+    """Expert picks of n_iter consecutive mini-batches whose per-expert load
+    drifts: iteration i draws from P(e) ~ (rank_i(e) + 1)^-s_i with s_i going
+    linearly from s_start to s_end (imbalance that fades as training goes on)
+    and two experts adjacent in the ranking swapping places every swap_every
+    iterations (popularity that moves between experts).  Returns a list of
+    [T,k] int32 arrays, k distinct picks per token."""
+    rng = _rng(seed, "traj", 0)
+    rank = rng.permutation(E)
+    out = []
+    for i in range(n_iter):
+        if i and swap_every and i % swap_every == 0 and E > 1:
+            a = int(rng.integers(0, E - 1))
+            rank[[a, a + 1]] = rank[[a + 1, a]]
+        s = s_start + (s_end - s_start) * (i / max(1, n_iter - 1))
+        p = np.empty(E)
+        p[rank] = (np.arange(1, E + 1, dtype=np.float64)) ** (-s)
+        p /= p.sum()
+        out.append(_sample_distinct(_rng(seed, "traj", i + 1), p, T, k))
+    return out
+
+
+def reassign_some(seed: int, ids: np.ndarray, E: int, frac: float) -> np.ndarray:
+    """A copy of [T,k] picks in which a seeded random subset of round(frac*T)
+    tokens gets fresh picks drawn uniformly (k distinct; a redraw can repeat
+    the old set by chance)."""
+    T, k = ids.shape
+    rng = _rng(seed, "reassign", 0)
+    out = np.array(ids, dtype=np.int32, copy=True)
+    n = int(round(frac * T))
+    if n:
+        who = rng.choice(T, size=n, replace=False)
+        out[who] = _sample_distinct(rng, np.full(E, 1.0 / E), n, k)
+    return out
