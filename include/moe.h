@@ -6,7 +6,9 @@
  * using Dynamic Recompilations" (MLSys 2022): Algorithm 1 (top-k MoE
  * forward), Eq. 1 (weighted sum of expert outputs), Eq. 4 and Section 3.1
  * (expert capacity, drops, dynamic capacity factors), Section 3.2 (sample
- * assignment caching).
+ * assignment caching), Eq. 3 (balance term), Eq. 2 and its appendix
+ * (specification loss, AggregateSpec), Section 3 with its implementation
+ * appendix (metric-driven changes at the launch frontier).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -15,7 +17,8 @@
  *   ready when the stream reaches that point.
  * - Pointers are DEVICE pointers unless a parameter is marked [host].  The
  *   caller owns all memory, including scratch `workspace` buffers sized by
- *   the matching *_workspace_bytes query.  The library keeps no state.
+ *   the matching *_workspace_bytes query.  The library keeps no state
+ *   beyond the capacity-policy objects the caller creates and destroys.
  * - Argument errors (bad sizes, NULL pointers, unsupported combinations,
  *   a workspace that is too small) are reported synchronously through the
  *   returned moe_status and nothing is enqueued.  Errors that depend on
@@ -243,16 +246,20 @@ size_t moe_gate_bwd_workspace_bytes(int T, int d, int E);
  *   raw (renorm = 0): g_j = dweights[t,j]
  *   renorm:           g_j = (dweights_j - sum_i dweights_i w_i) / S,
  *                     S = sum_j p[ids_j], w_j = p[ids_j]/S
- *   dp[t,e] = sum_j [ids[t,j] = e] g_j;  dlogits = p * (dp - <dp, p>)
+ *   dp[t,e] = sum_j [ids[t,j] = e] g_j (+ dprob_coef[e]);
+ *   dlogits = p * (dp - <dp, p>)
  *   dw_g[e,i] = sum_t dlogits[t,e] x[t,i]  (float32, fixed summation order)
  *   logits [T,E] (moe_gate_topk output), ids [T,k], dweights [T,k]
+ *   dprob_coef [E] float32 or NULL: a gradient with respect to the
+ *            probabilities that is the same for every token, such as the
+ *            balance term's (moe_balance_fwd)
  *   dlogits [T,E] f32 out, dw_g [E,d] f32 out (fully overwritten).
  */
 moe_status moe_gate_bwd(void* stream, moe_dtype dt, int T, int d, int E, int k,
                         int renorm, const void* x, const float* logits,
                         const int32_t* ids, const float* dweights,
-                        float* dlogits, float* dw_g, void* workspace,
-                        size_t workspace_bytes);
+                        const float* dprob_coef, float* dlogits, float* dw_g,
+                        void* workspace, size_t workspace_bytes);
 
 /*
  * moe_dispatch_bwd - backward of moe_dispatch plus the gate's input term:
@@ -264,6 +271,163 @@ moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d, int E,
                             int k, int64_t rows_alloc, const void* dx_disp,
                             const int32_t* dest_row, const float* dlogits,
                             const void* w_g, void* dx);
+
+/* ---- loss-side operators ------------------------------------------------ */
+
+/* Workspace bytes of moe_balance_fwd. [host] */
+size_t moe_balance_workspace_bytes(int T, int E);
+
+/*
+ * moe_balance_fwd - the balance term of Eq. 3, B = lambda * n * sum_i T_i G_i
+ * over the n = E experts, with T_i = counts[i] / (T k) (the share of the
+ * batch's assignments the gate gives expert i, counted before capacity) and
+ * G_i = mean over the T tokens of softmax(logits[t])[i].  T_i comes from an
+ * arg-top-k and has no gradient, so dB/dp[t,i] = lambda n T_i / T for every
+ * token; pass dprob_coef to moe_gate_bwd to add it to the gate gradient.
+ *   lambda     >= 0, finite (the regulariser's weight)
+ *   logits     [T,E] float32 (moe_gate_topk output)
+ *   counts     [E] int32 (moe_count / moe_dispatch output)
+ *   loss       [1] float32 out: B (0 for T = 0)
+ *   dprob_coef [E] float32 out: lambda n T_i / T
+ * Sums run in a fixed order (per-256-token partials in the workspace, then
+ * float64), so both outputs are deterministic.
+ */
+moe_status moe_balance_fwd(void* stream, int T, int E, int k, float lambda,
+                           const float* logits, const int32_t* counts,
+                           float* loss, float* dprob_coef, void* workspace,
+                           size_t workspace_bytes);
+
+/*
+ * moe_aggregate_spec - the AggregateSpec operator of the specification-loss
+ * appendix: the prediction of every (token, choice) pair, concatenated.
+ *   out [T*k, d] layer dtype: row t*k + j = y_disp[dest_row[t,j]] when that
+ *       assignment was kept, zeros when it was dropped (fully overwritten).
+ */
+moe_status moe_aggregate_spec(void* stream, moe_dtype dt, int T, int d, int k,
+                              const void* y_disp, const int32_t* dest_row,
+                              int64_t rows_alloc, void* out);
+
+/* Workspace bytes of moe_spec_loss. [host] */
+size_t moe_spec_loss_workspace_bytes(int T);
+
+/*
+ * moe_spec_loss - the specification loss of Eq. 2 with the squared error as
+ * the task loss, L(y, o) = (1/d) sum_c (o_c - y_c)^2, averaged over tokens,
+ * and both of its gradients, in one pass over the expert rows:
+ *   loss          = (1/T) sum_t sum_{j kept} w[t,j] L(target[t], O[t,j])
+ *   dweights[t,j] = L(target[t], O[t,j]) / T   (0 for a dropped assignment)
+ *   dy_disp[r]    = w[t,j] * 2 (O[t,j] - target[t]) / (T d)   for r = dest_row[t,j]
+ * with O[t,j] = y_disp[dest_row[t,j]].  A dropped assignment has no
+ * prediction and takes no part.  dy_disp feeds moe_expert_ffn_bwd and
+ * dweights feeds moe_gate_bwd, in place of moe_combine_bwd's outputs.
+ *   target   [T,d] layer dtype;  weights [T,k] float32 (the combine weights)
+ *   dy_disp  [rows_alloc,d] out: kept rows written, other rows untouched
+ *   dweights [T,k] float32 out;  loss [1] float32 out (0 for T = 0)
+ */
+moe_status moe_spec_loss(void* stream, moe_dtype dt, int T, int d, int k,
+                         const void* y_disp, const int32_t* dest_row,
+                         const float* weights, const void* target,
+                         int64_t rows_alloc, void* dy_disp, float* dweights,
+                         float* loss, void* workspace, size_t workspace_bytes);
+
+/* ---- sample assignment caching (Section 3.2) ------------------------------ */
+
+/*
+ * moe_cache_update - the Cache operator on one mini-batch: counts the
+ * samples whose set of picked experts in fresh_ids equals the set cached for
+ * them (order within a row does not matter), adds that number to
+ * *unchanged, and writes fresh_ids to cache_out for the next epoch.
+ *   fresh_ids [T,k] int32 (moe_gate_topk output)
+ *   cached    [T,k] int32: the previous epoch's picks of these samples
+ *   cache_out [T,k] int32 out: may be `cached` itself (in place); a separate
+ *             buffer (one per epoch parity) lets the cached picks stay
+ *             readable by the dispatch and the gate backward of the same
+ *             iteration without ordering this call after them
+ *   unchanged [1] int32 device counter, accumulated (the caller zeroes it at
+ *             the start of an epoch); an integer sum, so deterministic
+ */
+moe_status moe_cache_update(void* stream, int T, int k, const int32_t* fresh_ids,
+                            const int32_t* cached, int32_t* cache_out,
+                            int32_t* unchanged);
+
+/*
+ * moe_cached_weights - combine weights for cached picks from the gate's
+ * fresh scores: weights[t,j] = p[t, ids[t,j]], renorm != 0 divides by the
+ * sum over the row's picks, p = softmax(logits[t]).  Evaluated exactly as
+ * moe_gate_topk evaluates its weights, so picks equal to the gate's give
+ * bit-identical weights.  An id outside [0,E) gets weight 0.
+ *   logits [T,E] float32;  ids [T,k] int32;  weights [T,k] float32 out
+ */
+moe_status moe_cached_weights(void* stream, int T, int E, int k, int renorm,
+                              const float* logits, const int32_t* ids,
+                              float* weights);
+
+/*
+ * moe_caching_decision - the caching switch with hysteresis of Section 5.2:
+ * off -> on when unchanged/samples >= on_num/on_den and epoch >= min_epoch;
+ * on -> off when unchanged/samples < off_num/off_den (exact integer
+ * comparison).  The paper's setting is 96/100, 90/100, epoch 10.  Returns
+ * the new state (0 or 1), the old one for samples = 0, or -1 for invalid
+ * arguments (a denominator <= 0, negative values, unchanged > samples).
+ * [host]
+ */
+int moe_caching_decision(int enabled, int64_t unchanged, int64_t samples,
+                         int epoch, int on_num, int on_den, int off_num,
+                         int off_den, int min_epoch);
+
+/* ---- capacity policy at the launch frontier (Section 3, Section 3.1) ------ */
+
+/*
+ * A host object that turns the per-expert assignment counts of past
+ * iterations (the model metric) into per-expert capacities for the next
+ * launch, without stalling the device.  Owned by the caller: create,
+ * then per iteration moe_policy_begin before the launches that read the
+ * capacities and moe_policy_end after the launch that produces the counts;
+ * destroy at the end.  Not thread-safe; one stream per object.  It issues
+ * host-device copies, so keep it out of HIP graph capture.
+ *
+ * Trigger (run on the host): with the counts c of iteration i - 1 - delta,
+ * recompile when some c_e exceeds its capacity (drops) or some capacity
+ * exceeds ceil(shrink c_e) clamped to [cap_min, T]; a recompile sets every
+ * C_e = ceil(grow c_e) clamped to [cap_min, T].  Iterations 0..delta run
+ * with init_cap.
+ *
+ * moe_policy_create: delta_launch in [0, 64] (iterations launched ahead of
+ *   the metric the trigger sees); grow = grow_num/grow_den <= shrink =
+ *   shrink_num/shrink_den, all in [1, 10^6]; init_cap [host] [E] >= 0.
+ *   Allocates pinned host memory and events.  *out = NULL on error.
+ * moe_policy_begin: waits (host) until at most delta_launch iterations are
+ *   outstanding, runs the trigger on each metric consumed, and enqueues on
+ *   `stream` the upload of capacity [E] and offsets [E+1] (exclusive prefix
+ *   sum) when they changed or the buffers differ from the last call.
+ *   *rows_needed [host, optional] = sum of the capacities (the rows the
+ *   dispatch needs); *recompiled [host, optional] = 1 if the capacities
+ *   changed.  EINVAL when called twice without moe_policy_end.
+ * moe_policy_end: enqueues on `stream` the copy of counts [E] (device) into
+ *   the pinned ring and the event that marks it done.
+ * moe_policy_state [host]: current capacities cap [E] (optional), iterations
+ *   launched and consumed, recompiles so far.
+ */
+typedef struct moe_capacity_policy moe_capacity_policy;
+
+/* The trigger alone, as the policy runs it: updates cap [host] [E] in place
+ * from counts [host] [E]; returns 1 if it recompiled, 0 if not, -1 for
+ * invalid arguments. [host] */
+int moe_capacity_trigger(int T, int E, const int32_t* counts, int32_t* cap,
+                         int grow_num, int grow_den, int shrink_num,
+                         int shrink_den, int cap_min);
+
+moe_status moe_policy_create(int T, int k, int E, int delta_launch, int grow_num,
+                             int grow_den, int shrink_num, int shrink_den,
+                             int cap_min, const int32_t* init_cap,
+                             moe_capacity_policy** out);
+void moe_policy_destroy(moe_capacity_policy* p);
+moe_status moe_policy_begin(moe_capacity_policy* p, void* stream, int32_t* capacity,
+                            int32_t* offsets, int64_t* rows_needed, int* recompiled);
+moe_status moe_policy_end(moe_capacity_policy* p, void* stream, const int32_t* counts);
+moe_status moe_policy_state(const moe_capacity_policy* p, int32_t* cap,
+                            int64_t* launched, int64_t* consumed,
+                            int64_t* recompiles);
 
 /*
  * Kernel timing (instrumentation; not part of the method).  While enabled,

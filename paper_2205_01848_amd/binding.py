@@ -45,9 +45,28 @@ SIGNATURES = {
                                     _c_size]),
     "moe_gate_bwd_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int]),
     "moe_gate_bwd": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _p, _p,
-                              _p, _p, _p, _p, _p, _c_size]),
+                              _p, _p, _p, _p, _p, _p, _c_size]),
     "moe_dispatch_bwd": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_int, _c_i64, _p,
                                   _p, _p, _p, _p]),
+    "moe_balance_workspace_bytes": (_c_size, [_c_int, _c_int]),
+    "moe_balance_fwd": (_c_int, [_p, _c_int, _c_int, _c_int, ctypes.c_float, _p, _p, _p, _p,
+                                 _p, _c_size]),
+    "moe_aggregate_spec": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _p, _p, _c_i64, _p]),
+    "moe_spec_loss_workspace_bytes": (_c_size, [_c_int]),
+    "moe_spec_loss": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _p, _p, _p, _p, _c_i64, _p,
+                               _p, _p, _p, _c_size]),
+    "moe_cache_update": (_c_int, [_p, _c_int, _c_int, _p, _p, _p, _p]),
+    "moe_cached_weights": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _p, _p, _p]),
+    "moe_caching_decision": (_c_int, [_c_int, _c_i64, _c_i64, _c_int, _c_int, _c_int, _c_int,
+                                      _c_int, _c_int]),
+    "moe_capacity_trigger": (_c_int, [_c_int, _c_int, _p, _p, _c_int, _c_int, _c_int, _c_int,
+                                      _c_int]),
+    "moe_policy_create": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                   _c_int, _c_int, _p, _p]),
+    "moe_policy_destroy": (None, [_p]),
+    "moe_policy_begin": (_c_int, [_p, _p, _p, _p, _p, _p]),
+    "moe_policy_end": (_c_int, [_p, _p, _p]),
+    "moe_policy_state": (_c_int, [_p, _p, _p, _p, _p]),
     "moe_timing_enable": (_c_int, [_c_int]),
     "moe_timing_report": (_c_int, [ctypes.c_char_p, _c_size]),
 }
@@ -185,13 +204,13 @@ def moe_gate_bwd_workspace_bytes(T, d, E) -> int:
     return lib().moe_gate_bwd_workspace_bytes(T, d, E)
 
 
-def moe_gate_bwd(x, logits, ids, dweights, renorm, dlogits, dw_g, ws):
+def moe_gate_bwd(x, logits, ids, dweights, renorm, dlogits, dw_g, ws, dprob_coef=None):
     T, d = x.shape
     E = logits.shape[1]
     k = ids.shape[1]
     _check(lib().moe_gate_bwd(_stream(), _dt(x), T, d, E, k, int(renorm), _ptr(x), _ptr(logits),
-                              _ptr(ids), _ptr(dweights), _ptr(dlogits), _ptr(dw_g), _ptr(ws),
-                              ws.numel()), "moe_gate_bwd")
+                              _ptr(ids), _ptr(dweights), _ptr(dprob_coef), _ptr(dlogits),
+                              _ptr(dw_g), _ptr(ws), ws.numel()), "moe_gate_bwd")
 
 
 def moe_dispatch_bwd(dx_disp, dest_row, E, dlogits, w_g, dx):
@@ -200,6 +219,115 @@ def moe_dispatch_bwd(dx_disp, dest_row, E, dlogits, w_g, dx):
     _check(lib().moe_dispatch_bwd(_stream(), _dt(dx), T, d, E, k, dx_disp.shape[0],
                                   _ptr(dx_disp), _ptr(dest_row), _ptr(dlogits), _ptr(w_g),
                                   _ptr(dx)), "moe_dispatch_bwd")
+
+
+# ---- loss-side operators ------------------------------------------------------
+def moe_balance_workspace_bytes(T, E) -> int:
+    return lib().moe_balance_workspace_bytes(T, E)
+
+
+def moe_balance_fwd(logits, counts, k, lam, loss, dprob_coef, ws):
+    T, E = logits.shape
+    _check(lib().moe_balance_fwd(_stream(), T, E, k, float(lam), _ptr(logits), _ptr(counts),
+                                 _ptr(loss), _ptr(dprob_coef), _ptr(ws), ws.numel()),
+           "moe_balance_fwd")
+
+
+def moe_aggregate_spec(y_disp, dest_row, out):
+    T, k = dest_row.shape
+    d = out.shape[1]
+    _check(lib().moe_aggregate_spec(_stream(), _dt(out), T, d, k, _ptr(y_disp), _ptr(dest_row),
+                                    y_disp.shape[0], _ptr(out)), "moe_aggregate_spec")
+
+
+def moe_spec_loss_workspace_bytes(T) -> int:
+    return lib().moe_spec_loss_workspace_bytes(T)
+
+
+def moe_spec_loss(y_disp, dest_row, weights, target, dy_disp, dweights, loss, ws):
+    T, k = dest_row.shape
+    d = target.shape[1]
+    _check(lib().moe_spec_loss(_stream(), _dt(target), T, d, k, _ptr(y_disp), _ptr(dest_row),
+                               _ptr(weights), _ptr(target), y_disp.shape[0], _ptr(dy_disp),
+                               _ptr(dweights), _ptr(loss), _ptr(ws), ws.numel()),
+           "moe_spec_loss")
+
+
+# ---- sample assignment caching ------------------------------------------------
+def moe_cache_update(fresh_ids, cached, cache_out, unchanged):
+    T, k = fresh_ids.shape
+    _check(lib().moe_cache_update(_stream(), T, k, _ptr(fresh_ids), _ptr(cached), _ptr(cache_out),
+                                  _ptr(unchanged)), "moe_cache_update")
+
+
+def moe_cached_weights(logits, ids, renorm, weights):
+    T, E = logits.shape
+    k = ids.shape[1]
+    _check(lib().moe_cached_weights(_stream(), T, E, k, int(renorm), _ptr(logits), _ptr(ids),
+                                    _ptr(weights)), "moe_cached_weights")
+
+
+def moe_caching_decision(enabled, unchanged, samples, epoch, on=(96, 100), off=(90, 100),
+                         min_epoch=10) -> bool:
+    r = lib().moe_caching_decision(int(bool(enabled)), int(unchanged), int(samples), int(epoch),
+                                   on[0], on[1], off[0], off[1], int(min_epoch))
+    if r < 0:
+        raise MoEError("moe_caching_decision: invalid arguments")
+    return bool(r)
+
+
+# ---- capacity policy at the launch frontier --------------------------------------
+def moe_capacity_trigger(T, counts, cap, grow, shrink, cap_min=0):
+    """Host trigger: returns (new capacities, recompiled)."""
+    E = len(counts)
+    c = (ctypes.c_int32 * E)(*[int(v) for v in counts])
+    C = (ctypes.c_int32 * E)(*[int(v) for v in cap])
+    r = lib().moe_capacity_trigger(T, E, c, C, grow[0], grow[1], shrink[0], shrink[1], cap_min)
+    if r < 0:
+        raise MoEError("moe_capacity_trigger: invalid arguments")
+    return list(C), bool(r)
+
+
+class CapacityPolicy:
+    """Owner of one moe_capacity_policy object (see include/moe.h)."""
+
+    def __init__(self, T, k, E, delta_launch, grow, shrink, init_cap, cap_min=0):
+        init = (ctypes.c_int32 * E)(*[int(c) for c in init_cap])
+        h = ctypes.c_void_p()
+        _check(lib().moe_policy_create(T, k, E, delta_launch, grow[0], grow[1], shrink[0],
+                                       shrink[1], cap_min, init, ctypes.byref(h)),
+               "moe_policy_create")
+        self._h, self.E = h, E
+
+    def begin(self, capacity, offsets):
+        """Enqueue the capacities for the next launch; returns (rows needed,
+        whether the trigger recompiled)."""
+        rows = ctypes.c_int64()
+        rec = ctypes.c_int()
+        _check(lib().moe_policy_begin(self._h, _stream(), _ptr(capacity), _ptr(offsets),
+                                      ctypes.byref(rows), ctypes.byref(rec)), "moe_policy_begin")
+        return rows.value, bool(rec.value)
+
+    def end(self, counts):
+        _check(lib().moe_policy_end(self._h, _stream(), _ptr(counts)), "moe_policy_end")
+
+    def state(self):
+        cap = (ctypes.c_int32 * self.E)()
+        n, c, r = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().moe_policy_state(self._h, cap, ctypes.byref(n), ctypes.byref(c),
+                                      ctypes.byref(r)), "moe_policy_state")
+        return dict(cap=list(cap), launched=n.value, consumed=c.value, recompiles=r.value)
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            lib().moe_policy_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 # ---- kernel timing (instrumentation) ----------------------------------------

@@ -17,7 +17,7 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmoe.so")
-SOURCES = ["capi.hip", "gate.hip", "route.hip", "ffn.hip"]
+SOURCES = ["capi.hip", "gate.hip", "route.hip", "ffn.hip", "losses.hip", "cache.hip", "policy.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

@@ -1,11 +1,13 @@
 // Gate of the MoE layer: linear scores, softmax, top-k and normalised
 // weights (Algorithm 1, first three steps), and their backward.
 //
-// bf16 forward: one wavefront scores 32 tokens against up to 64 experts with
+// bf16 forward: one workgroup scores 32 tokens against up to 64 experts with
 // v_mfma_f32_32x32x16_bf16 (token rows as the A operand, expert rows of w_g
-// as the B operand, both K-contiguous); x is streamed from HBM exactly once
-// with 64-byte contiguous runs per lane, so the kernel is HBM-bound.
+// as the B operand, both K-contiguous), its four waves splitting K; x is
+// streamed from HBM exactly once, so the kernel is HBM-bound.
 // fp32 forward: one thread per token with float32 FMAs (small layers only).
+
+#include <type_traits>
 
 #include "common.hpp"
 #include "validate.hpp"
@@ -50,19 +52,29 @@ __device__ __forceinline__ void finish_token(const float* l, int E, int k,
   }
 }
 
-constexpr int kGateTokPerWave = 32;
-constexpr int kGateWaves = 4;
+constexpr int kGateTile = 32;   // tokens per MFMA row tile
+constexpr int kGateWaves = 4;   // waves per workgroup
 
-template <int NT>  // expert tiles of 32 (E <= 32*NT)
+// A workgroup scores kGateWaves / S token tiles of 32 tokens; the S waves of
+// one tile split K: wave w of the tile takes the 64-wide K steps w, w+S,
+// w+2S, ..., each wave keeping U steps of loads in flight.  S = 1 suits long
+// batches (each wave streams whole rows, U = 1 measured fastest there);
+// small batches take S = 2 or 4 (with U = 2) so the grid still fills the
+// chip.  The S partial scores are summed through LDS in a fixed order.
+template <int NT, int U>  // expert tiles of 32 (E <= 32*NT); K steps per load batch
 __global__ __launch_bounds__(256) void gate_fwd_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wg,
     const float* __restrict__ bias, int T, int d, int E, int k, int renorm,
-    float* __restrict__ logits, int32_t* __restrict__ ids,
+    int S, float* __restrict__ logits, int32_t* __restrict__ ids,
     float* __restrict__ weights) {
-  __shared__ float sl[kGateWaves][kGateTokPerWave][65];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  constexpr int P = NT * 32 + 1;  // LDS row pitch (floats)
+  __shared__ float part[kGateWaves][kGateTile][P];
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int lane = threadIdx.x & 63;
   const int r = lane & 31, half = lane >> 5;
-  const int t0 = (blockIdx.x * kGateWaves + wave) * kGateTokPerWave;
+  const int tiles = kGateWaves / S;
+  const int tile = wave / S, split = wave - tile * S;
+  const int t0 = (blockIdx.x * tiles + tile) * kGateTile;
   int trow = t0 + r;
   if (trow >= T) trow = T - 1;  // clamp loads; results of such rows are not stored
   const uint16_t* xr = x + static_cast<size_t>(trow) * d;
@@ -77,55 +89,75 @@ __global__ __launch_bounds__(256) void gate_fwd_bf16_kernel(
   for (int nt = 0; nt < NT; ++nt)
     for (int i = 0; i < 16; ++i) acc[nt][i] = 0.f;
 
-  // K mapping shared by both operands: lane half h, MFMA i, element q
-  // carries k = kb + 32h + 8i + q.
-  for (int kb = 0; kb < d; kb += 64) {
-    uint4 av[4];
-    uint4 bv[NT][4];
+  // K mapping shared by both operands: step s, lane half h, MFMA i, element
+  // q carries k = 64 s + 32 h + 8 i + q.
+  const int nsteps = (d + 63) / 64;
+  for (int s0 = split; s0 < nsteps; s0 += S * U) {
+    uint4 av[U][4];
+    uint4 bv[U][NT][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int kk = kb + half * 32 + i * 8;
-      const bool ok = kk < d;
-      av[i] = ok ? *reinterpret_cast<const uint4*>(xr + kk) : make_uint4(0, 0, 0, 0);
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const bool okb = ok && (nt * 32 + r) < E;
-        bv[nt][i] = okb ? *reinterpret_cast<const uint4*>(wr[nt] + kk) : make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < 4; ++i) {
+        const int kk = (s0 + u * S) * 64 + half * 32 + i * 8;
+        const bool ok = kk < d;
+        av[u][i] = ok ? *reinterpret_cast<const uint4*>(xr + kk) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const bool okb = ok && (nt * 32 + r) < E;
+          bv[u][nt][i] = okb ? *reinterpret_cast<const uint4*>(wr[nt] + kk) : make_uint4(0, 0, 0, 0);
+        }
       }
-    }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      bf16x8 a = __builtin_bit_cast(bf16x8, av[i]);
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        bf16x8 b = __builtin_bit_cast(bf16x8, bv[nt][i]);
-        acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[nt], 0, 0, 0);
+      for (int i = 0; i < 4; ++i) {
+        bf16x8 a = __builtin_bit_cast(bf16x8, av[u][i]);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          bf16x8 b = __builtin_bit_cast(bf16x8, bv[u][nt][i]);
+          acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[nt], 0, 0, 0);
+        }
       }
-    }
   }
   // accumulator layout: register q holds row (q/4)*8 + 4*half + q%4, column r
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const int n = nt * 32 + r;
-    if (n < E) {
-      const float b = bias ? bias[n] : 0.f;
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int row = (q >> 2) * 8 + half * 4 + (q & 3);
-        sl[wave][row][n] = acc[nt][q] + b;
-      }
+    for (int q = 0; q < 16; ++q) {
+      const int row = (q >> 2) * 8 + half * 4 + (q & 3);
+      part[wave][row][nt * 32 + r] = acc[nt][q];
     }
   }
   __syncthreads();
-  // logits out, coalesced along E
-  for (int idx = lane; idx < kGateTokPerWave * E; idx += 64) {
+  // sum each tile's K partials in split order, add the bias; logits out,
+  // coalesced along E
+  const int tb = blockIdx.x * tiles * kGateTile;
+  for (int idx = threadIdx.x; idx < tiles * kGateTile * E; idx += 256) {
     const int row = idx / E, e = idx - row * E;
-    if (t0 + row < T) logits[static_cast<size_t>(t0 + row) * E + e] = sl[wave][row][e];
+    const int tt = row / kGateTile, rr = row - tt * kGateTile;
+    float v = part[tt * S][rr][e];
+    for (int w = 1; w < S; ++w) v += part[tt * S + w][rr][e];
+    v += bias ? bias[e] : 0.f;
+    part[tt * S][rr][e] = v;
+    if (tb + row < T) logits[static_cast<size_t>(tb + row) * E + e] = v;
   }
-  if (lane < kGateTokPerWave && t0 + lane < T) {
-    const size_t t = t0 + lane;
-    finish_token(&sl[wave][lane][0], E, k, renorm, ids + t * k, weights + t * k);
+  __syncthreads();
+  const int row = threadIdx.x;
+  if (row < tiles * kGateTile && tb + row < T) {
+    const int tt = row / kGateTile, rr = row - tt * kGateTile;
+    const size_t t = tb + row;
+    finish_token(&part[tt * S][rr][0], E, k, renorm, ids + t * k, weights + t * k);
   }
+}
+
+// Waves per token tile: 1 while the grid has at least 512 workgroups, else
+// as many (2 or 4) as it takes to reach that or the maximum.
+inline int gate_split(int T) {
+  int S = 1;
+  while (S < kGateWaves && (T + kGateTile * (kGateWaves / S) - 1) / (kGateTile * (kGateWaves / S)) < 512)
+    S *= 2;
+  return S;
 }
 
 __global__ __launch_bounds__(64) void gate_fwd_f32_kernel(
@@ -155,8 +187,8 @@ __global__ __launch_bounds__(64) void gate_fwd_f32_kernel(
 // dlogits per token (thread per token).
 __global__ __launch_bounds__(64) void gate_bwd_dlogits_kernel(
     const float* __restrict__ logits, const int32_t* __restrict__ ids,
-    const float* __restrict__ dweights, int T, int E, int k, int renorm,
-    float* __restrict__ dlogits) {
+    const float* __restrict__ dweights, const float* __restrict__ coef, int T, int E, int k,
+    int renorm, float* __restrict__ dlogits) {
   __shared__ float sp[64][65];
   __shared__ float sdp[64][65];
   const int lane = threadIdx.x;
@@ -174,7 +206,7 @@ __global__ __launch_bounds__(64) void gate_bwd_dlogits_kernel(
   const float inv = 1.f / s;
   for (int e = 0; e < E; ++e) {
     sp[lane][e] *= inv;
-    sdp[lane][e] = 0.f;
+    sdp[lane][e] = coef ? coef[e] : 0.f;  // a dprobs term shared by every token
   }
   const int32_t* id = ids + static_cast<size_t>(t) * k;
   const float* dw = dweights + static_cast<size_t>(t) * k;
@@ -284,16 +316,21 @@ extern "C" moe_status moe_gate_topk(void* stream, moe_dtype dt, int T, int d,
   hipStream_t s = static_cast<hipStream_t>(stream);
   MOE_TIMED("gate_fwd", s);
   if (dt == MOE_BF16) {
-    const int tok_per_block = kGateTokPerWave * kGateWaves;
+    const int S = gate_split(T);
+    const int tok_per_block = kGateTile * (kGateWaves / S);
     dim3 grid((T + tok_per_block - 1) / tok_per_block);
-    if (E <= 32)
-      gate_fwd_bf16_kernel<1><<<grid, 256, 0, s>>>(
-          static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_g), bias,
-          T, d, E, k, renorm, logits, ids, weights);
-    else
-      gate_fwd_bf16_kernel<2><<<grid, 256, 0, s>>>(
-          static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_g), bias,
-          T, d, E, k, renorm, logits, ids, weights);
+    auto go = [&](auto nt, auto u) {
+      gate_fwd_bf16_kernel<decltype(nt)::value, decltype(u)::value><<<grid, 256, 0, s>>>(
+          static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_g), bias, T, d, E,
+          k, renorm, S, logits, ids, weights);
+    };
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    if (E <= 32) {
+      if (S == 1) go(I1{}, I1{}); else go(I1{}, I2{});
+    } else {
+      if (S == 1) go(I2{}, I1{}); else go(I2{}, I2{});
+    }
   } else {
     gate_fwd_f32_kernel<<<dim3((T + 63) / 64), 64, 0, s>>>(
         static_cast<const float*>(x), static_cast<const float*>(w_g), bias, T, d,
@@ -312,8 +349,8 @@ extern "C" size_t moe_gate_bwd_workspace_bytes(int T, int d, int E) {
 extern "C" moe_status moe_gate_bwd(void* stream, moe_dtype dt, int T, int d,
                                    int E, int k, int renorm, const void* x,
                                    const float* logits, const int32_t* ids,
-                                   const float* dweights, float* dlogits,
-                                   float* dw_g, void* workspace,
+                                   const float* dweights, const float* dprob_coef,
+                                   float* dlogits, float* dw_g, void* workspace,
                                    size_t workspace_bytes) {
   if (!dtype_ok(dt) || !shape_ok(T, E, k) || !width_ok(d)) return MOE_EINVAL;
   if (!dw_g) return MOE_EINVAL;
@@ -333,8 +370,9 @@ extern "C" moe_status moe_gate_bwd(void* stream, moe_dtype dt, int T, int d,
   const int nchunks = (T + kGbTok - 1) / kGbTok;
   {
     MOE_TIMED("gate_bwd_dlogits", s);
-    gate_bwd_dlogits_kernel<<<dim3((T + 63) / 64), 64, 0, s>>>(logits, ids, dweights, T, E,
-                                                             k, renorm, dlogits);
+    gate_bwd_dlogits_kernel<<<dim3((T + 63) / 64), 64, 0, s>>>(logits, ids, dweights,
+                                                             dprob_coef, T, E, k, renorm,
+                                                             dlogits);
     MOE_LAUNCH_CHECK();
   }
   dim3 grid((E + 7) / 8, (d + 511) / 512, nchunks);

@@ -13,6 +13,8 @@
 // one wavefront per token, 16-byte vector loads/stores along the row, so x
 // is read once even when k rows are written.
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "validate.hpp"
 
@@ -325,48 +327,81 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
   }
 }
 
-// dx[t] = sum_j kept dx_disp[r_j] (+ dl[t] . w_g).  Tokens are processed
-// kTokGroup at a time per wavefront so each w_g vector is loaded once per
-// group rather than once per token.
-constexpr int kTokGroup = 4;
+// dx[t] = sum_j kept dx_disp[r_j] (+ dl[t] . w_g).  A wavefront takes a group
+// of TG tokens (k <= KT) and one 64-vector column chunk of their rows
+// (blockIdx.y), so each w_g vector is loaded once per group rather than once
+// per token, and issues all of the group's row gathers at once.
+template <int KT> struct DispatchBwdShape {
+  static constexpr int TG = KT <= 2 ? 8 : 16 / KT;   // tokens per wavefront
+};
 
-template <typename T, bool GATE>
+template <typename T, bool GATE, int KT>
 __global__ __launch_bounds__(256) void dispatch_bwd_kernel(
     const uint4* __restrict__ dxd, const int32_t* __restrict__ dest_row,
     const float* __restrict__ dl, const uint4* __restrict__ wg, int Ttok, int E, int k,
     int nvec, int64_t rows_alloc, uint4* __restrict__ dx) {
   constexpr int V = Elem<T>::kVec;
-  const int tg = (blockIdx.x * kRowWaves + (threadIdx.x >> 6)) * kTokGroup;
+  constexpr int kTokGroup = DispatchBwdShape<KT>::TG;
+  constexpr int kMaxK = KT;
+  // wave-uniform token group: its routing values and dlogits come in through
+  // scalar loads, read once per group rather than once per row vector
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int tg = (static_cast<int>(blockIdx.x) * kRowWaves + wave) * kTokGroup;
   const int lane = threadIdx.x & 63;
   if (tg >= Ttok) return;
-  for (int v = lane; v < nvec; v += 64) {
+  int rows[kTokGroup][kMaxK];
+#pragma unroll
+  for (int u = 0; u < kTokGroup; ++u)
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+      int r = -1;
+      if (j < k && tg + u < Ttok) r = dest_row[static_cast<size_t>(tg + u) * k + j];
+      rows[u][j] = r >= 0 && r < rows_alloc ? r : -1;
+    }
+  const int v = static_cast<int>(blockIdx.y) * 64 + lane;
+  if (v >= nvec) return;
+  {
     float acc[kTokGroup][V];
+    // issue every gather of the group before summing
+    uint4 raw[kTokGroup][kMaxK];
+#pragma unroll
+    for (int u = 0; u < kTokGroup; ++u)
+#pragma unroll
+      for (int j = 0; j < kMaxK; ++j)
+        if (j < k && rows[u][j] >= 0) raw[u][j] = dxd[static_cast<size_t>(rows[u][j]) * nvec + v];
 #pragma unroll
     for (int u = 0; u < kTokGroup; ++u) {
 #pragma unroll
       for (int i = 0; i < V; ++i) acc[u][i] = 0.f;
-      const int t = tg + u;
-      if (t >= Ttok) continue;
-      for (int j = 0; j < k; ++j) {
-        const int r = dest_row[static_cast<size_t>(t) * k + j];
-        if (r >= 0 && r < rows_alloc) {
+#pragma unroll
+      for (int j = 0; j < kMaxK; ++j)
+        if (j < k && rows[u][j] >= 0) {
           float f[V];
-          Elem<T>::load(dxd[static_cast<size_t>(r) * nvec + v], f);
+          Elem<T>::load(raw[u][j], f);
 #pragma unroll
           for (int i = 0; i < V; ++i) acc[u][i] += f[i];
         }
-      }
     }
     if constexpr (GATE) {
-      for (int e = 0; e < E; ++e) {
-        float f[V];
-        Elem<T>::load(wg[static_cast<size_t>(e) * nvec + v], f);
+      // four w_g vectors in flight per step
+      constexpr int kEu = 4;
+      for (int e0 = 0; e0 < E; e0 += kEu) {
+        uint4 gv[kEu];
 #pragma unroll
-        for (int u = 0; u < kTokGroup; ++u) {
-          const int t = tg + u;
-          const float g = t < Ttok ? dl[static_cast<size_t>(t) * E + e] : 0.f;
+        for (int q = 0; q < kEu; ++q)
+          if (e0 + q < E) gv[q] = wg[static_cast<size_t>(e0 + q) * nvec + v];
 #pragma unroll
-          for (int i = 0; i < V; ++i) acc[u][i] = fmaf(g, f[i], acc[u][i]);
+        for (int q = 0; q < kEu; ++q) {
+          if (e0 + q >= E) break;
+          float f[V];
+          Elem<T>::load(gv[q], f);
+#pragma unroll
+          for (int u = 0; u < kTokGroup; ++u) {
+            const int t = tg + u;
+            const float g = t < Ttok ? dl[static_cast<size_t>(t) * E + e0 + q] : 0.f;
+#pragma unroll
+            for (int i = 0; i < V; ++i) acc[u][i] = fmaf(g, f[i], acc[u][i]);
+          }
         }
       }
     }
@@ -526,22 +561,29 @@ extern "C" moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d,
   if (!aligned16(dx_disp) || !aligned16(dx) || (w_g && !aligned16(w_g))) return MOE_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
-  const int grid = nblocks(T, kRowWaves * kTokGroup);
   const uint4* a = static_cast<const uint4*>(dx_disp);
   const uint4* g = static_cast<const uint4*>(w_g);
   uint4* o = static_cast<uint4*>(dx);
   MOE_TIMED("dispatch_bwd", s);
-  if (dt == MOE_BF16) {
-    if (dlogits)
-      dispatch_bwd_kernel<uint16_t, true><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
-    else
-      dispatch_bwd_kernel<uint16_t, false><<<grid, 256, 0, s>>>(a, dest_row, nullptr, nullptr, T, E, k, nvec, rows_alloc, o);
-  } else {
-    if (dlogits)
-      dispatch_bwd_kernel<float, true><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
-    else
-      dispatch_bwd_kernel<float, false><<<grid, 256, 0, s>>>(a, dest_row, nullptr, nullptr, T, E, k, nvec, rows_alloc, o);
-  }
+  auto go = [&](auto kt_tag) {
+    constexpr int KT = decltype(kt_tag)::value;
+    const dim3 grid(nblocks(T, kRowWaves * DispatchBwdShape<KT>::TG), nblocks(nvec, 64));
+    if (dt == MOE_BF16) {
+      if (dlogits)
+        dispatch_bwd_kernel<uint16_t, true, KT><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
+      else
+        dispatch_bwd_kernel<uint16_t, false, KT><<<grid, 256, 0, s>>>(a, dest_row, nullptr, nullptr, T, E, k, nvec, rows_alloc, o);
+    } else {
+      if (dlogits)
+        dispatch_bwd_kernel<float, true, KT><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
+      else
+        dispatch_bwd_kernel<float, false, KT><<<grid, 256, 0, s>>>(a, dest_row, nullptr, nullptr, T, E, k, nvec, rows_alloc, o);
+    }
+  };
+  if (k <= 1) go(std::integral_constant<int, 1>{});
+  else if (k <= 2) go(std::integral_constant<int, 2>{});
+  else if (k <= 4) go(std::integral_constant<int, 4>{});
+  else go(std::integral_constant<int, 8>{});
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }

@@ -79,6 +79,11 @@ class MoELayer:
                 self.dlogits = e(T, E, t=f32)
                 self.dw_g = e(E, d, t=f32)
                 self.ws_gate_bwd = B.workspace(B.moe_gate_bwd_workspace_bytes(T, d, E), self.dev)
+        # loss-side operators and caching: allocated on first use
+        self.balance_loss = self.dprob_coef = self.ws_balance = None
+        self._balance_on = False
+        self.spec_loss_value = self.ws_spec = None
+        self.cached_weights = None
 
     # ---- forward pieces ------------------------------------------------------
     def gate(self, x, w_g, bias, renorm: int):
@@ -110,6 +115,37 @@ class MoELayer:
         B.moe_combine(self.y_disp, self.dest_row, self.weights if weights is None else weights,
                       self.y)
 
+    # ---- loss-side operators ----------------------------------------------------
+    def balance(self, lam: float):
+        """Eq. 3 balance term of this batch from the gate logits and the
+        demand counts of the last dispatch; keeps its dprobs coefficient for
+        the gate backward.  Returns the [1] loss tensor."""
+        if self.balance_loss is None:
+            self.balance_loss = torch.empty(1, dtype=torch.float32, device=self.dev)
+            self.dprob_coef = torch.empty(self.E, dtype=torch.float32, device=self.dev)
+            self.ws_balance = B.workspace(B.moe_balance_workspace_bytes(self.T, self.E), self.dev)
+        B.moe_balance_fwd(self.logits, self.counts, self.k, lam, self.balance_loss,
+                          self.dprob_coef, self.ws_balance)
+        self._balance_on = True
+        return self.balance_loss
+
+    def aggregate_spec(self, out: Optional[torch.Tensor] = None):
+        """AggregateSpec: [T*k, d] predictions of every (token, choice)."""
+        if out is None:
+            out = torch.empty(self.T * self.k, self.d, dtype=self.dtype, device=self.dev)
+        B.moe_aggregate_spec(self.y_disp, self.dest_row, out)
+        return out
+
+    def spec_loss(self, target, weights: Optional[torch.Tensor] = None):
+        """Eq. 2 with squared error: the [1] loss, with dy_disp and dweights
+        written for the backward (in place of combine_bwd)."""
+        if self.spec_loss_value is None:
+            self.spec_loss_value = torch.empty(1, dtype=torch.float32, device=self.dev)
+            self.ws_spec = B.workspace(B.moe_spec_loss_workspace_bytes(self.T), self.dev)
+        B.moe_spec_loss(self.y_disp, self.dest_row, self.weights if weights is None else weights,
+                        target, self.dy_disp, self.dweights, self.spec_loss_value, self.ws_spec)
+        return self.spec_loss_value
+
     # ---- backward pieces -----------------------------------------------------
     def combine_bwd(self, dy, weights: Optional[torch.Tensor] = None):
         B.moe_combine_bwd(dy, self.y_disp, self.dest_row,
@@ -124,7 +160,8 @@ class MoELayer:
 
     def gate_bwd(self, x, renorm: int, ids: Optional[torch.Tensor] = None):
         B.moe_gate_bwd(x, self.logits, self.ids if ids is None else ids, self.dweights, renorm,
-                       self.dlogits, self.dw_g, self.ws_gate_bwd)
+                       self.dlogits, self.dw_g, self.ws_gate_bwd,
+                       dprob_coef=self.dprob_coef if self._balance_on else None)
 
     def dispatch_bwd(self, w_g=None):
         if w_g is not None:
@@ -133,31 +170,82 @@ class MoELayer:
             B.moe_dispatch_bwd(self.dx_disp, self.dest_row, self.E, None, None, self.dx)
 
     # ---- whole layer ---------------------------------------------------------
-    def forward(self, x, w1, w3, w2, *, w_g=None, bias=None, renorm=0, ids=None, weights=None,
-                capacity=("dynamic", 1, 1), counts_from_batch=True, rows="fill"):
-        """gate (or cached ids) -> [count ->] capacity -> dispatch -> FFN -> combine.
-
-        capacity = ("static", num, den) | ("dynamic", num, den); a dynamic rule
-        uses this batch's counts when counts_from_batch, else the counts left
-        in self.counts by the previous dispatch (a lagged capacity update)."""
-        if ids is None:
-            self.gate(x, w_g, bias, renorm)
-            ids, weights = self.ids, self.weights
+    def _capacity(self, capacity, ids, counts_from_batch):
         kind, num, den = capacity
         if kind == "static":
             self.capacity_static(num, den)
+        elif kind == "policy":
+            pass            # capacity and offsets uploaded by a CapacityPolicy
         else:
             if counts_from_batch:
                 self.count(ids)
             self.capacity_dynamic(num, den)
+
+    def forward(self, x, w1, w3, w2, *, w_g=None, bias=None, renorm=0, ids=None, weights=None,
+                capacity=("dynamic", 1, 1), counts_from_batch=True, rows="fill",
+                balance: Optional[float] = None):
+        """gate (or cached ids) -> [count ->] capacity -> dispatch -> FFN -> combine.
+
+        capacity = ("static", num, den) | ("dynamic", num, den) | ("policy",
+        1, 1); a dynamic rule uses this batch's counts when counts_from_batch,
+        else the counts left in self.counts by the previous dispatch (a lagged
+        capacity update); "policy" uses capacities a CapacityPolicy uploaded.
+        balance = lambda adds the Eq. 3 balance term (self.balance_loss) and
+        its gradient to the gate backward."""
+        self._balance_on = False
+        if ids is None:
+            self.gate(x, w_g, bias, renorm)
+            ids, weights = self.ids, self.weights
+        self._capacity(capacity, ids, counts_from_batch)
         self.dispatch(x, ids)
+        if balance is not None:
+            self.balance(balance)
         self.ffn_fwd(w1, w3, w2, rows=rows)
         self.combine(weights)
         return self.y
 
+    def forward_cached(self, x, w1, w3, w2, *, cached, cache_out, unchanged, w_g, bias=None,
+                       renorm=0, capacity=("dynamic", 1, 1), gate_stream=None, rows="fill"):
+        """Forward with sample assignment caching on (Section 3.2): the expert
+        batches are built from the cached picks while the gate runs on
+        gate_stream; the combine waits for the gate and weighs the cached
+        picks with the fresh probabilities.  The Cache operator counts the
+        samples whose picks did not change (added to `unchanged`) and writes
+        the fresh picks to cache_out, which must not be `cached` when the gate
+        runs on another stream.  Backward: ids=cached,
+        weights=self.cached_weights."""
+        main = torch.cuda.current_stream(self.dev)
+        gs = gate_stream if gate_stream is not None else main
+        if gs is not main and cache_out.data_ptr() == cached.data_ptr():
+            raise ValueError("cache_out must differ from cached when the gate runs concurrently")
+        if self.cached_weights is None:
+            self.cached_weights = torch.empty(self.T, self.k, dtype=torch.float32,
+                                              device=self.dev)
+        self._balance_on = False
+        ready = torch.cuda.Event()
+        ready.record(main)
+        with torch.cuda.stream(gs):
+            gs.wait_event(ready)
+            self.gate(x, w_g, bias, renorm)
+            B.moe_cached_weights(self.logits, cached, renorm, self.cached_weights)
+            B.moe_cache_update(self.ids, cached, cache_out, unchanged)
+            gate_done = torch.cuda.Event()
+            gate_done.record(gs)
+        self._capacity(capacity, cached, True)
+        self.dispatch(x, cached)
+        self.ffn_fwd(w1, w3, w2, rows=rows)
+        main.wait_event(gate_done)
+        self.combine(self.cached_weights)
+        return self.y
+
     def backward(self, x, dy, w1, w3, w2, *, w_g=None, renorm=0, ids=None, weights=None,
-                 rows="fill"):
-        self.combine_bwd(dy, self.weights if weights is None else weights)
+                 rows="fill", target=None):
+        """combine_bwd (or, given target, the Eq. 2 specification loss in its
+        place) -> FFN backward -> gate backward -> dispatch backward."""
+        if target is not None:
+            self.spec_loss(target, self.weights if weights is None else weights)
+        else:
+            self.combine_bwd(dy, self.weights if weights is None else weights)
         self.ffn_bwd(w1, w3, w2, rows=rows)
         if w_g is not None:
             self.gate_bwd(x, renorm, ids)

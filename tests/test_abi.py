@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared_functions():
         assert hasattr(lib, name), name
         assert name in B.SIGNATURES, f"binding lacks {name}"
-    assert lib.moe_abi_version() == 2
+    assert lib.moe_abi_version() == 3
     assert lib.moe_status_string(0) == b"MOE_OK"
 
 
@@ -112,5 +112,52 @@ def test_combine_and_backward_reject_bad_arguments():
     # dlogits without w_g
     assert L.moe_dispatch_bwd(None, 1, 10, 64, 4, 2, 100, FAKE, FAKE, FAKE, None, FAKE) == EINVAL
     assert L.moe_gate_bwd_workspace_bytes(100, 64, 4) > 0
-    assert L.moe_gate_bwd(None, 1, 100, 64, 4, 2, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                          0) == EWORKSPACE
+    assert L.moe_gate_bwd(None, 1, 100, 64, 4, 2, 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                          FAKE, 0) == EWORKSPACE
+
+
+def test_loss_operators_reject_bad_arguments():
+    L = B.lib()
+    need = L.moe_balance_workspace_bytes(1000, 8)
+    assert need >= 4 * 8 * 4       # four 256-token partials of 8 experts
+    assert L.moe_balance_workspace_bytes(1000, 65) == 0
+    assert L.moe_balance_fwd(None, 1000, 8, 2, ctypes.c_float(-0.1), FAKE, FAKE, FAKE, FAKE, FAKE,
+                             need) == EINVAL
+    assert L.moe_balance_fwd(None, 1000, 8, 2, ctypes.c_float(float("nan")), FAKE, FAKE, FAKE,
+                             FAKE, FAKE, need) == EINVAL
+    assert L.moe_balance_fwd(None, 1000, 8, 2, ctypes.c_float(float("inf")), FAKE, FAKE, FAKE,
+                             FAKE, FAKE, need) == EINVAL
+    assert L.moe_balance_fwd(None, 1000, 8, 2, ctypes.c_float(0.01), FAKE, FAKE, FAKE, FAKE, FAKE,
+                             need - 1) == EWORKSPACE
+    assert L.moe_aggregate_spec(None, 1, 10, 64, 0, FAKE, FAKE, 100, FAKE) == EINVAL      # k = 0
+    assert L.moe_aggregate_spec(None, 1, 10, 60, 2, FAKE, FAKE, 100, FAKE) == EINVAL      # d % 8
+    wsl = L.moe_spec_loss_workspace_bytes(10)
+    assert L.moe_spec_loss(None, 1, 10, 64, 2, FAKE, FAKE, FAKE, FAKE, 100, FAKE, FAKE, FAKE,
+                           FAKE, wsl - 1) == EWORKSPACE
+    assert L.moe_spec_loss(None, 1, 10, 64, 2, FAKE, FAKE, FAKE, None, 100, FAKE, FAKE, FAKE,
+                           FAKE, wsl) == EINVAL                                            # target
+
+
+def test_cache_operators_reject_bad_arguments():
+    L = B.lib()
+    assert L.moe_cache_update(None, 10, 9, FAKE, FAKE, FAKE, FAKE) == EINVAL             # k > 8
+    assert L.moe_cache_update(None, 10, 2, FAKE, FAKE, FAKE, None) == EINVAL
+    assert L.moe_cached_weights(None, 10, 65, 2, 1, FAKE, FAKE, FAKE) == EINVAL           # E > 64
+    assert L.moe_cached_weights(None, 10, 8, 2, 1, None, FAKE, FAKE) == EINVAL
+    assert L.moe_caching_decision(0, 5, 4, 20, 96, 100, 90, 100, 10) == -1               # u > n
+    assert L.moe_caching_decision(0, 5, 10, 20, 96, 0, 90, 100, 10) == -1                # den 0
+
+
+def test_policy_rejects_bad_arguments():
+    L = B.lib()
+    init = (ctypes.c_int32 * 4)(5, 5, 5, 5)
+    h = ctypes.c_void_p()
+    # grow above shrink, negative delta, bad ratio, negative initial capacity
+    assert L.moe_policy_create(100, 2, 4, 1, 14, 10, 13, 10, 0, init, ctypes.byref(h)) == EINVAL
+    assert L.moe_policy_create(100, 2, 4, -1, 11, 10, 13, 10, 0, init, ctypes.byref(h)) == EINVAL
+    assert L.moe_policy_create(100, 2, 4, 1, 0, 10, 13, 10, 0, init, ctypes.byref(h)) == EINVAL
+    neg = (ctypes.c_int32 * 4)(5, -1, 5, 5)
+    assert L.moe_policy_create(100, 2, 4, 1, 11, 10, 13, 10, 0, neg, ctypes.byref(h)) == EINVAL
+    assert not h.value
+    assert L.moe_policy_begin(None, None, FAKE, FAKE, None, None) == EINVAL
+    assert L.moe_policy_end(None, None, FAKE) == EINVAL

@@ -154,7 +154,8 @@ def test_padded_static_rows_match_on_filled_rows():
 
 
 # ---- combine, combine backward, dispatch backward -----------------------------
-@pytest.mark.parametrize("dt,k,d", [("bf16", 2, 512), ("f32", 1, 64), ("bf16", 3, 136)])
+@pytest.mark.parametrize("dt,k,d", [("bf16", 2, 512), ("f32", 1, 64), ("bf16", 3, 136),
+                                    ("bf16", 5, 1096), ("f32", 2, 584)])
 def test_combine_and_backward(dt, k, d):
     rng = np.random.default_rng(50 + k)
     T, E = 1500, 6
@@ -165,7 +166,9 @@ def test_combine_and_backward(dt, k, d):
     R = int(off[-1])
     s = O.assign_slots(ids, E, cap, off, R)
     dest = s["dest_row"]
-    assert (dest < 0).any() and ((dest < 0).all(axis=1)).any()
+    assert (dest < 0).any()
+    if k <= 3:     # with 5 picks of 6 experts every token keeps one
+        assert ((dest < 0).all(axis=1)).any()
     wts = rng.random((T, k)).astype(np.float32)
     yd = _enc(rng.standard_normal((R, d)), dt)
     dy = _enc(rng.standard_normal((T, d)), dt)

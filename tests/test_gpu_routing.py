@@ -34,6 +34,9 @@ def _run_gate(x_np, wg_np, b_np, k, renorm, dt):
     (333, 64, 33, 3, 1, "bf16"),
     (70, 200, 16, 8, 1, "bf16"),
     (1, 8, 1, 1, 0, "bf16"),
+    # long batches: two waves per token tile, then one (whole rows per wave)
+    (40001, 72, 8, 2, 1, "bf16"),
+    (70001, 136, 40, 2, 1, "bf16"),
     (129, 64, 4, 1, 0, "f32"),
     (300, 40, 64, 4, 1, "f32"),
 ])
