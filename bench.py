@@ -32,6 +32,14 @@ DESCR = {
     "c4": "T=32768 d=2048 E=32 top-2 d_ff=8192 ReLU bf16 cached Zipf(1.2) assignments, exact capacity, forward+backward",
     "c5": "T=65536 d=4096 E=8 top-2 d_ff=14336 SwiGLU bf16, dynamic capacity 1.05, forward+backward",
 }
+VARIANTS = {
+    "balance": "with the Eq. 3 balance term and its gate gradient",
+    "spec": "with AggregateSpec and the Eq. 2 specification loss (squared error) driving "
+            "the backward",
+    "cached": "sample assignment caching on: dispatch and FFN from cached picks (4% of "
+              "samples reassigned) while the gate runs on a second stream",
+    "policy": "capacities from the host launch-frontier policy (pinned counts ring)",
+}
 # bounded oracle sample (tokens) per workload, about 10-30 s of CPU work
 CPU_SAMPLE = {"c1": 256, "c2": 8192, "c3": 16384, "c4": 2048, "c5": 512}
 
@@ -50,6 +58,18 @@ def parse():
                     help="override: static:num/den or dynamic:num/den")
     ap.add_argument("--rows", default="fill", choices=["fill", "capacity"],
                     help="capacity = padded static-shape baseline")
+    ap.add_argument("--variant", default="base", choices=["base", "balance", "spec", "cached",
+                                                          "policy"],
+                    help="base: the layer step; balance: + Eq. 3 balance term and its gate "
+                         "gradient; spec: + AggregateSpec, backward driven by the Eq. 2 "
+                         "specification loss; cached: caching on, gate on a second stream; "
+                         "policy: capacities from the host launch-frontier policy")
+    ap.add_argument("--lam", type=float, default=0.01, help="balance term weight")
+    ap.add_argument("--delta", type=int, default=1, help="policy: delta_launch")
+    ap.add_argument("--policy-sweep", action="store_true",
+                    help="instead of the layer: routing-only run of a drifting trajectory "
+                         "of mini-batches, drops vs average capacity factor for static "
+                         "capacities and for launch-frontier policies")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead of the layer: time a plain device-to-device copy of this "
@@ -102,6 +122,12 @@ def hbm_bytes(wl, kept, active):
             (T * E * 4 + E * d * s if wl.gate == "linear" else 0)
     if wl.gate != "linear":
         del b["gate_fwd"]
+    # operators of the variants
+    b["balance_fwd"] = T * E * 4 + E * 4
+    b["aggregate_spec"] = kept * d * s + T * k * d * s + T * k * 4
+    b["spec_loss"] = 2 * kept * d * s + T * d * s + T * k * 12
+    b["cache_update"] = 3 * T * k * 4
+    b["cached_weights"] = T * E * 4 + 2 * T * k * 4
     return b
 
 
@@ -159,6 +185,103 @@ def cpu_baseline(wl, I, cap_rule, ntok):
                       f"({el:.1f} s)"}
 
 
+def policy_sweep(args):
+    """Drops vs average capacity factor over a drifting trajectory of
+    mini-batches (routing only: count -> capacity -> dispatch of narrow
+    rows), for static capacities (Eq. 4) and launch-frontier policies
+    (Section 3.1 with the recompile appendix), every capacity trajectory
+    checked against the oracle's simulation on the same counts."""
+    import numpy as np
+    import torch
+
+    import oracle as O
+    import workloads as W
+    from paper_2205_01848_amd import binding as B
+
+    wl = W.config(args.workload)
+    T, E, k, N, dw = wl.T, wl.E, wl.k, args.steps, 8
+    log(f"policy sweep on {args.workload} shapes: {N} drifting mini-batches")
+    traj = W.drifting_assignments(wl.seed, T, E, k, N)
+    seq = [O.count_assignments(a, E) for a in traj]
+    dev = torch.device("cuda:0")
+    ids_dev = [torch.from_numpy(a).to(dev) for a in traj]
+    R = E * T
+    x = torch.zeros(T, dw, dtype=torch.bfloat16, device=dev)
+    cap = torch.empty(E, dtype=torch.int32, device=dev)
+    off = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    counts = torch.empty(E, dtype=torch.int32, device=dev)
+    fill = torch.empty(E, dtype=torch.int32, device=dev)
+    dest = torch.empty(T, k, dtype=torch.int32, device=dev)
+    src = torch.empty(R, dtype=torch.int32, device=dev)
+    xd = torch.empty(R, dw, dtype=torch.bfloat16, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    ws = B.workspace(B.moe_dispatch_workspace_bytes(T, E, k), dev)
+    fills = torch.empty(N, E, dtype=torch.int32, device=dev)
+    caps = torch.empty(N, E, dtype=torch.int32, device=dev)
+    demand = float(T * k)
+
+    def summarise(name, extra):
+        torch.cuda.synchronize()
+        f = fills.cpu().numpy().astype(np.int64)
+        c = caps.cpu().numpy().astype(np.int64)
+        drops = (np.array(seq) - f).sum()
+        row = {"setting": name, "dropped_pct": round(100.0 * drops / (N * demand), 3),
+               "avg_capacity_factor": round(float(c.sum(axis=1).mean()) / demand, 4)}
+        row.update(extra)
+        return row, c
+
+    rows = []
+    for a in [(1, 1), (5, 4), (3, 2), (2, 1), (3, 1)]:
+        for i in range(N):
+            B.moe_update_capacity(T, k, E, None, a[0], a[1], 0, cap, off)
+            B.moe_dispatch(x, ids_dev[i], E, cap, off, R, counts, fill, dest, src, xd, status, ws)
+            fills[i].copy_(fill)
+            caps[i].copy_(cap)
+        rows.append(summarise(f"static alpha {a[0]}/{a[1]}", {})[0])
+    for margin in [(21, 20), (11, 10)]:
+        for i in range(N):
+            B.moe_count(ids_dev[i], E, counts, status)
+            B.moe_update_capacity(T, k, E, counts, margin[0], margin[1], 0, cap, off)
+            B.moe_dispatch(x, ids_dev[i], E, cap, off, R, counts, fill, dest, src, xd, status, ws)
+            fills[i].copy_(fill)
+            caps[i].copy_(cap)
+        rows.append(summarise(f"device dynamic {margin[0]}/{margin[1]} (this batch's counts)",
+                              {})[0])
+    init = O.capacity_static(T, k, E, 1, 1)
+    ok = True
+    for grow, shrink in [((21, 20), (5, 4)), ((11, 10), (13, 10)), ((6, 5), (3, 2)),
+                         ((5, 4), (2, 1))]:
+        for delta in (0, 1, 2):
+            pol = B.CapacityPolicy(T, k, E, delta, grow, shrink, init)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(N):
+                pol.begin(cap, off)
+                B.moe_dispatch(x, ids_dev[i], E, cap, off, R, counts, fill, dest, src, xd,
+                               status, ws)
+                pol.end(counts)
+                fills[i].copy_(fill)
+                caps[i].copy_(cap)
+            torch.cuda.synchronize()
+            wall = (time.perf_counter() - t0) * 1e3 / N
+            st = pol.state()
+            pol.close()
+            row, c = summarise(f"policy grow {grow[0]}/{grow[1]} shrink {shrink[0]}/{shrink[1]} "
+                               f"delta {delta}",
+                               {"recompiles": st["recompiles"], "ms_per_iteration": round(wall, 3)})
+            sim = O.simulate_capacity_policy(seq, T, k, delta, init, grow, shrink)
+            match = bool(np.array_equal(c, sim["caps"]))
+            ok = ok and match
+            row["oracle_caps_match"] = match
+            rows.append(row)
+    out = {"metric": "capacity policy: dropped assignments vs average capacity factor",
+           "workload": f"{args.workload} shapes T={T} E={E} k={k}, {N} mini-batches with "
+                       "drifting Zipf loads (exponent 1.2 -> 0.6, adjacent experts swap "
+                       "every 5)",
+           "status": int(status.item()), "all_policies_match_oracle": ok, "rows": rows}
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -167,6 +290,9 @@ def main():
         sys.exit(2)
     if args.copy_gib > 0:
         copy_calibration(args.copy_gib, args.steps)
+        return
+    if args.policy_sweep:
+        policy_sweep(args)
         return
     import numpy as np
     import torch
@@ -207,13 +333,58 @@ def main():
         fkw = dict(ids=up(I.ids), weights=up(I.cw))
         bkw = dict(weights=fkw["weights"])
 
-    def step():
-        L.forward(x, w1, w3, w2, capacity=cap_rule, rows=args.rows, **fkw)
-        if wl.backward:
-            L.backward(x, dy, w1, w3, w2, rows=args.rows, **bkw)
+    variant = args.variant
+    if variant in ("balance", "cached") and wl.gate != "linear":
+        raise SystemExit(f"--variant {variant} needs a workload with a gate")
+    if variant in ("balance", "spec", "cached") and not wl.backward:
+        raise SystemExit(f"--variant {variant} needs a training workload")
+    extra = {}
+    if variant == "spec":
+        extra["target"] = up(W.make_target(wl))
+        extra["spec_rows"] = torch.empty(wl.T * wl.k, wl.d, dtype=td, device=dev)
+    if variant == "cached":
+        # last epoch's picks: the gate's own, with 4% of the samples reassigned
+        L.gate(x, fkw["w_g"], fkw["bias"], wl.renorm)
+        fresh = L.ids.cpu().numpy()
+        extra["cached"] = torch.from_numpy(W.reassign_some(wl.seed, fresh, wl.E, 0.04)).to(dev)
+        extra["cache_out"] = torch.empty_like(extra["cached"])
+        extra["unchanged"] = torch.zeros(1, dtype=torch.int32, device=dev)
+        extra["gate_stream"] = torch.cuda.Stream()
+    if variant == "policy":
+        T_, k_, E_ = wl.T, wl.k, wl.E
+        init = [-(-T_ * k_ // E_)] * E_                 # Eq. 4 with alpha = 1
+        grow = (cap_rule[1], cap_rule[2]) if cap_rule[0] == "dynamic" else (21, 20)
+        extra["policy"] = B.CapacityPolicy(T_, k_, E_, args.delta, grow, (5, 4), init)
+        extra["recompiles"] = 0
 
+    def step():
+        if variant == "cached":
+            L.forward_cached(x, w1, w3, w2, cached=extra["cached"], cache_out=extra["cache_out"],
+                             unchanged=extra["unchanged"], w_g=fkw["w_g"], bias=fkw["bias"],
+                             renorm=wl.renorm, capacity=cap_rule, gate_stream=extra["gate_stream"],
+                             rows=args.rows)
+            L.backward(x, dy, w1, w3, w2, rows=args.rows, ids=extra["cached"],
+                       weights=L.cached_weights, **bkw)
+            return
+        if variant == "policy":
+            rows_needed, _ = extra["policy"].begin(L.capacity, L.offsets)
+            if rows_needed > L.rows_alloc:
+                raise SystemExit(f"policy asks for {rows_needed} rows > {L.rows_alloc}")
+            L.forward(x, w1, w3, w2, capacity=("policy", 1, 1), rows=args.rows, **fkw)
+            extra["policy"].end(L.counts)
+        else:
+            L.forward(x, w1, w3, w2, capacity=cap_rule, rows=args.rows,
+                      balance=args.lam if variant == "balance" else None, **fkw)
+        if variant == "spec":
+            L.aggregate_spec(extra["spec_rows"])
+        if wl.backward:
+            L.backward(x, dy, w1, w3, w2, rows=args.rows, target=extra.get("target"), **bkw)
+
+    warmup = args.warmup
+    if variant == "policy":
+        warmup = max(warmup, args.delta + 2)    # the first recompile has taken effect
     log("warmup")
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     log("timed steps")
@@ -281,14 +452,16 @@ def main():
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": warmup,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {DESCR[args.workload]}", "T": wl.T, "d": wl.d,
+        "config": {"workload": f"{args.workload}: {DESCR[args.workload]}"
+                   + ("" if variant == "base" else f" [{VARIANTS[variant]}]"),
+                   "T": wl.T, "d": wl.d,
                    "E": wl.E, "k": wl.k, "d_ff": wl.f, "act": wl.act,
                    "capacity": f"{cap_rule[0]} {cap_rule[1]}/{cap_rule[2]}",
                    "rows": args.rows, "pass": "fwd+bwd" if wl.backward else "fwd",
@@ -300,6 +473,23 @@ def main():
                    "gemm_share": round(gemm_ms / total_ms, 4),
                    "input_gen_s": round(t_gen, 1), "kernels": detail},
     }
+    if variant != "base":
+        out["config"]["variant"] = variant
+    if variant == "balance":
+        out["config"]["lambda"] = args.lam
+        out["detail"]["balance_loss"] = float(L.balance_loss.item())
+    if variant == "spec":
+        out["detail"]["spec_loss"] = float(L.spec_loss_value.item())
+    if variant == "cached":
+        n = warmup + args.steps
+        out["detail"]["unchanged_fraction"] = round(
+            int(extra["unchanged"].item()) / (n * wl.T), 4)
+    if variant == "policy":
+        st = extra["policy"].state()
+        out["detail"]["policy"] = {"delta_launch": args.delta, "recompiles": st["recompiles"],
+                                   "capacity": st["cap"],
+                                   "capacity_factor": round(sum(st["cap"]) / (wl.T * wl.k), 4)}
+        extra["policy"].close()
     print(json.dumps(out))
 
 

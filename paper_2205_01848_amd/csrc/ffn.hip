@@ -80,6 +80,28 @@ template <> __device__ __forceinline__ void load_vec<float>(const char* p, float
   v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
+// 8 elements as raw bits (one 16-byte vector of bf16, two of fp32), so a
+// load can be issued early and decoded later.
+template <typename T> struct Raw8 {
+  uint4 v[sizeof(T) / 2];
+  __device__ __forceinline__ void load(const char* p) {
+#pragma unroll
+    for (int i = 0; i < static_cast<int>(sizeof(T) / 2); ++i)
+      v[i] = reinterpret_cast<const uint4*>(p)[i];
+  }
+  __device__ __forceinline__ void to_f(float* f) const {
+    if constexpr (sizeof(T) == 2) {
+      unpack8(v[0], f);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        f[4 * i + 0] = __uint_as_float(v[i].x); f[4 * i + 1] = __uint_as_float(v[i].y);
+        f[4 * i + 2] = __uint_as_float(v[i].z); f[4 * i + 3] = __uint_as_float(v[i].w);
+      }
+    }
+  }
+};
+
 // ---------------------------------------------------------------------------
 // activations (shared by forward epilogue, backward epilogue and transposes)
 // ---------------------------------------------------------------------------
@@ -618,6 +640,63 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
     // wave's own LDS strip, then each lane finishes 8 consecutive columns of
     // a row and writes them as one vector.
     const int wcol = wq * 64;   // the wave's first tile column
+    if constexpr (MODE == M_BWD_DA || MODE == M_BWD_DA_SWIGLU) {
+      // dH = dA act'(H): 16 (row block, strip half, row group) iterations,
+      // each reading 8 saved pre-activations (two planes for SwiGLU) per
+      // lane.  Those loads run kPf iterations ahead of their use, so the
+      // wave waits for HBM once per tile rather than once per iteration.
+      constexpr bool SW = MODE == M_BWD_DA_SWIGLU;
+      constexpr int kIt = 16, kPf = 4;
+      Raw8<T> q1[kIt], q3[kIt];
+      auto pos = [&](int n, int& lm, int& gc) {
+        const int i = n >> 2, h = (n >> 1) & 1, it = n & 1;
+        lm = team * 128 + i * 32 + h * 16 + it * 8 + (lane >> 3);
+        gc = n0 + wcol + (lane & 7) * 8;
+      };
+      auto issue = [&](int n) {
+        int lm, gc;
+        pos(n, lm, gc);
+        const bool ok = lm < m_valid && gc < p.N;
+        // out-of-tile lanes read the tile's first valid element instead
+        const int64_t o = static_cast<int64_t>(row0 + (ok ? lm : 0)) * p.ldh +
+                          static_cast<int64_t>(ok ? gc : n0) * ES;
+        q1[n].load(p.H1 + o);
+        if constexpr (SW) q3[n].load(p.H3 + o);
+      };
+#pragma unroll
+      for (int n = 0; n < kPf; ++n) issue(n);
+#pragma unroll
+      for (int n = 0; n < kIt; ++n) {
+        if (n + kPf < kIt) issue(n + kPf);
+        if ((n & 1) == 0) stage_strip(strip, acc, n >> 2, (n >> 1) & 1);
+        int lm, gc;
+        pos(n, lm, gc);
+        if (lm < m_valid && gc < p.N) {
+          const int r = (n & 1) * 8 + (lane >> 3), c8 = (lane & 7) * 8;
+          const int64_t grow = row0 + lm;
+          float h1[8], g1[8];
+          q1[n].to_f(h1);
+          if constexpr (SW) {
+            float h3[8], g3[8];
+            q3[n].to_f(h3);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float da = strip[r * kStripPitch + c8 + e];
+              const float sg = sigm(h1[e]);
+              g1[e] = da * h3[e] * sg * (1.f + h1[e] * (1.f - sg));
+              g3[e] = da * h1[e] * sg;
+            }
+            store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
+            store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(p.f + gc) * ES, g3);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              g1[e] = strip[r * kStripPitch + c8 + e] * act_grad_f(h1[e], p.act);
+            store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
+          }
+        }
+      }
+    } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -667,37 +746,6 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
               store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, v);
             }
           }
-        } else if constexpr (MODE == M_BWD_DA || MODE == M_BWD_DA_SWIGLU) {
-          constexpr bool SW = MODE == M_BWD_DA_SWIGLU;
-#pragma unroll
-          for (int it = 0; it < 2; ++it) {
-            const int r = it * 8 + (lane >> 3), c8 = (lane & 7) * 8;
-            const int lm = srow0 + r;
-            const int gc = n0 + wcol + c8;
-            if (lm < m_valid && gc < p.N) {
-              const int64_t grow = row0 + lm;
-              float h1[8], g1[8];
-              load_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h1);
-              if constexpr (SW) {
-                float h3[8], g3[8];
-                load_vec<T>(p.H3 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h3);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  const float da = strip[r * kStripPitch + c8 + e];
-                  const float sg = sigm(h1[e]);
-                  g1[e] = da * h3[e] * sg * (1.f + h1[e] * (1.f - sg));
-                  g3[e] = da * h1[e] * sg;
-                }
-                store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
-                store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(p.f + gc) * ES, g3);
-              } else {
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                  g1[e] = strip[r * kStripPitch + c8 + e] * act_grad_f(h1[e], p.act);
-                store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
-              }
-            }
-          }
         } else {  // M_DW: fp32 rows of dW (or of a partial-sum slot)
 #pragma unroll
           for (int it = 0; it < 2; ++it) {
@@ -724,6 +772,7 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
           }
         }
       }
+    }
     }
     __syncthreads();   // strips are free before the next tile's loads
   }

@@ -23,55 +23,57 @@ namespace {
 
 constexpr int kBalTok = 256;  // tokens per block of the probability sums
 
-// part[b][e] = sum over the block's tokens of softmax(logits[t])[e]
+// part[b][e] = sum over the block's tokens of softmax(logits[t])[e]: one
+// thread per token, column sums by wave shuffles, then the four waves in
+// order.
 __global__ __launch_bounds__(256) void balance_partial_kernel(
     const float* __restrict__ logits, int T, int E, float* __restrict__ part) {
-  __shared__ float sp[kBalTok][kMaxE + 1];
-  const int tid = threadIdx.x;
+  __shared__ float wsum[4][kMaxE];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int t = blockIdx.x * kBalTok + tid;
-  if (t < T) {
-    const float* l = logits + static_cast<size_t>(t) * E;
-    float m = -INFINITY;
-    for (int e = 0; e < E; ++e) m = fmaxf(m, l[e]);
-    float s = 0.f;
-    for (int e = 0; e < E; ++e) {
-      const float z = expf(l[e] - m);
-      sp[tid][e] = z;
-      s += z;
-    }
-    const float inv = 1.f / s;
-    for (int e = 0; e < E; ++e) sp[tid][e] *= inv;
-  } else {
-    for (int e = 0; e < E; ++e) sp[tid][e] = 0.f;
+  const float* l = logits + static_cast<size_t>(t < T ? t : 0) * E;
+  float m = -INFINITY;
+  for (int e = 0; e < E; ++e) m = fmaxf(m, l[e]);
+  float s = 0.f;
+  for (int e = 0; e < E; ++e) s += expf(l[e] - m);
+  const float inv = t < T ? 1.f / s : 0.f;
+  for (int e = 0; e < E; ++e) {
+    const float v = wave_sum(expf(l[e] - m) * inv);
+    if (lane == 0) wsum[wave][e] = v;
   }
   __syncthreads();
-  if (tid < E) {
-    float acc = 0.f;
-    for (int r = 0; r < kBalTok; ++r) acc += sp[r][tid];
-    part[static_cast<size_t>(blockIdx.x) * E + tid] = acc;
-  }
+  if (tid < E)
+    part[static_cast<size_t>(blockIdx.x) * E + tid] =
+        (wsum[0][tid] + wsum[1][tid]) + (wsum[2][tid] + wsum[3][tid]);
 }
 
-// G_e = sum_b part[b][e] / T; B = lambda n sum_e T_e G_e; c_e = lambda n T_e / T
-__global__ __launch_bounds__(64) void balance_finish_kernel(
+// G_e = sum_b part[b][e] / T; B = lambda n sum_e T_e G_e; c_e = lambda n T_e / T.
+// 256 threads: thread (g, e) sums the partials b = g, g + 4, ... of expert e.
+__global__ __launch_bounds__(256) void balance_finish_kernel(
     const float* __restrict__ part, int nblk, const int32_t* __restrict__ counts, int T,
     int E, int k, float lambda, float* __restrict__ loss, float* __restrict__ coef) {
+  __shared__ double acc4[4][kMaxE];
   __shared__ double term[kMaxE];
-  const int e = threadIdx.x;
+  const int e = threadIdx.x & 63, g = threadIdx.x >> 6;
   if (e < E) {
-    double g = 0.0;
-    for (int b = 0; b < nblk; ++b) g += part[static_cast<size_t>(b) * E + e];
+    double a = 0.0;
+    for (int b = g; b < nblk; b += 4) a += part[static_cast<size_t>(b) * E + e];
+    acc4[g][e] = a;
+  }
+  __syncthreads();
+  if (g == 0 && e < E) {
+    double G = (acc4[0][e] + acc4[1][e]) + (acc4[2][e] + acc4[3][e]);
     double tf = 0.0, c = 0.0;
     if (T > 0) {
-      g /= T;
+      G /= T;
       tf = static_cast<double>(counts[e]) / (static_cast<double>(T) * k);
       c = static_cast<double>(lambda) * E * tf / T;
     }
-    term[e] = tf * g;
+    term[e] = tf * G;
     coef[e] = static_cast<float>(c);
   }
   __syncthreads();
-  if (e == 0) {
+  if (threadIdx.x == 0) {
     double b = 0.0;
     for (int i = 0; i < E; ++i) b += term[i];
     *loss = static_cast<float>(static_cast<double>(lambda) * E * b);
@@ -211,7 +213,7 @@ extern "C" moe_status moe_balance_fwd(void* stream, int T, int E, int k, float l
     balance_partial_kernel<<<nb, 256, 0, s>>>(logits, T, E, part);
     MOE_LAUNCH_CHECK();
   }
-  balance_finish_kernel<<<1, 64, 0, s>>>(part, nb, counts, T, E, k, lambda, loss, dprob_coef);
+  balance_finish_kernel<<<1, 256, 0, s>>>(part, nb, counts, T, E, k, lambda, loss, dprob_coef);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }
