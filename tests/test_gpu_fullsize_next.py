@@ -1,0 +1,206 @@
+"""Full-size GPU parity, on the c5 layer (T=65536, d=4096, E=8, k=2,
+d_ff=14336, SwiGLU), of the operators beyond the core path, in the launch
+configuration bench.py's variants time:
+
+* balance term (Eq. 3): loss and dprobs coefficient against the oracle over
+  all tokens; the gate backward with it on sampled tokens;
+* AggregateSpec and the specification loss (Eq. 2): sampled (token,
+  choice) rows against the oracle's expert rows, dweights and dy_disp rows of
+  sampled tokens, and the loss against the sum the kernel's own dweights
+  imply (a property that holds at any size);
+* caching (Section 3.2): the unchanged-sample count over all tokens, the
+  weights at cached picks, and sampled layer outputs with the gate on a
+  second stream;
+* the capacity policy on device counts of c5-sized mini-batches.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import NEAR_TIE, RTOL, assert_close, dev, to_dev, to_np
+from paper_2205_01848_amd import MoELayer, rows_alloc_for
+from paper_2205_01848_amd import binding as B
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+
+class LazyF64:
+    """[E, a, b] bf16 weights as float64, one expert at a time on first use."""
+
+    def __init__(self, arr):
+        self.arr, self.shape, self.cache = arr, arr.shape, {}
+
+    def __getitem__(self, e):
+        e = int(e)
+        if e not in self.cache:
+            self.cache[e] = O.bf16_to_f64(self.arr[e])
+        return self.cache[e]
+
+
+@pytest.fixture(scope="module")
+def c5():
+    wl = W.config("c5")
+    I = W.make_inputs(wl)
+    X = O.bf16_to_f64(I.x)
+    logits = O.gate_logits(X, O.bf16_to_f64(I.w_g), I.bias)
+    return wl, I, X, logits
+
+
+def _layer(wl, I):
+    kind, num, den = wl.capacity[0]
+    R = rows_alloc_for(kind, wl.T, wl.k, wl.E, num, den)
+    L = MoELayer(wl.T, wl.d, wl.E, wl.k, wl.f, wl.act, torch.bfloat16, R, backward=True)
+    t = {n: to_dev(getattr(I, n), "bf16") for n in ("x", "w1", "w3", "w2", "w_g", "dy")}
+    t["bias"] = torch.from_numpy(I.bias).to(dev())
+    return L, R, t
+
+
+def _routing_ok(L, logits, wl):
+    """The kernel's picks, allowing certified near ties (see test_gpu_fullsize)."""
+    ids = O.topk(logits, wl.k).astype(np.int64)
+    got = to_np(L.ids)
+    tol = NEAR_TIE * float(np.abs(logits).max())
+    diff = np.nonzero((got != ids).any(axis=1))[0]
+    for t in diff:
+        assert tuple(int(v) for v in got[t]) in O.topk_alternatives(logits[t], wl.k, tol)
+        ids[t] = got[t]
+    assert len(diff) <= 4
+    return ids
+
+
+def _sample(dest, n, seed):
+    rng = np.random.default_rng(seed)
+    cand = np.nonzero((dest >= 0).any(axis=1))[0]
+    return np.sort(rng.choice(cand, size=min(n, len(cand)), replace=False))
+
+
+def test_balance_and_spec_loss_full_size(c5):
+    wl, I, X, logits = c5
+    L, R, t = _layer(wl, I)
+    lam = 0.01
+    tgt_np = W.make_target(wl)
+    tgt = to_dev(tgt_np, "bf16")
+    L.forward(t["x"], t["w1"], t["w3"], t["w2"], w_g=t["w_g"], bias=t["bias"], renorm=wl.renorm,
+              capacity=wl.capacity[0], balance=lam)
+    spec_rows = L.aggregate_spec()
+    L.backward(t["x"], None, t["w1"], t["w3"], t["w2"], w_g=t["w_g"], renorm=wl.renorm,
+               target=tgt)
+    torch.cuda.synchronize()
+
+    ids = _routing_ok(L, logits, wl)
+    counts = O.count_assignments(ids, wl.E)
+    np.testing.assert_array_equal(to_np(L.counts), counts)
+    Bref, coef = O.balance_term(logits, counts, wl.k, lam)
+    assert_close(to_np(L.balance_loss), np.array([Bref]), 1e-5, "balance loss")
+    assert_close(to_np(L.dprob_coef), coef, 1e-6, "dprob coefficient")
+
+    kind, num, den = wl.capacity[0]
+    cap = O.capacity_dynamic(counts, wl.T, num, den)
+    off = O.exclusive_offsets(cap)
+    s = O.assign_slots(ids, wl.E, cap, off, R)
+    dest = s["dest_row"]
+    np.testing.assert_array_equal(to_np(L.dest_row), dest)
+    wts = O.gate_weights(O.softmax(logits), ids, wl.renorm)
+
+    toks = _sample(dest, 40, 3)
+    tt, jj = np.nonzero(dest[toks] >= 0)
+    rows, rtok, e_of = dest[toks][tt, jj], toks[tt], ids[toks][tt, jj]
+    W1, W2, W3 = LazyF64(I.w1), LazyF64(I.w2), LazyF64(I.w3)
+    fr = O.ffn_rows_fwd(X[rtok], e_of, W1, W3, W2, wl.act, "bf16")
+    rt = RTOL["bf16"]
+    # AggregateSpec rows t*k + j: the expert rows, bit for bit the kernel's Y rows
+    sel = torch.from_numpy((rtok * wl.k + jj).astype(np.int64)).to(dev())
+    agg = to_np(spec_rows[sel])
+    np.testing.assert_array_equal(agg, to_np(L.y_disp[torch.from_numpy(rows.astype(np.int64)).to(dev())]))
+    assert_close(agg, fr["Y"], rt, "AggregateSpec rows")
+    # specification loss gradients on the sampled rows, from the oracle's Y
+    Tgt = O.bf16_to_f64(tgt_np)
+    dsub = -np.ones_like(dest[toks])
+    dsub[tt, jj] = np.arange(len(rows))
+    # unrounded oracle terms over the sample; T enters as the batch size, so
+    # rescale from len(toks) to T, then round dY once as the kernel does
+    _, dw_ref, dY_ref = O.spec_loss(fr["Y"], dsub, wts[toks], Tgt[toks], "f32")
+    scale = len(toks) / wl.T
+    assert_close(to_np(L.dweights)[toks], dw_ref * scale, rt, "spec dweights")
+    assert_close(to_np(L.dy_disp[torch.from_numpy(rows.astype(np.int64)).to(dev())]),
+                 O.round_bf16(dY_ref * scale), rt, "spec dy_disp rows")
+    # the loss is the w-weighted sum of the kernel's per-choice losses
+    dwg = to_np(L.dweights)
+    assert_close(to_np(L.spec_loss_value), np.array([(to_np(L.weights) * dwg).sum()]), 1e-5,
+                 "spec loss vs its dweights")
+    # gate backward with the balance coefficient, sampled tokens
+    dl_ref, _ = O.gate_bwd(logits[toks], ids[toks], dwg[toks], wl.renorm, X[toks],
+                           dprob_coef=to_np(L.dprob_coef))
+    assert_close(to_np(L.dlogits)[toks], dl_ref, 1e-5, "dlogits with balance term")
+
+
+def test_cached_forward_full_size(c5):
+    wl, I, X, logits = c5
+    ids_gate = O.topk(logits, wl.k)
+    cached = W.reassign_some(wl.seed, ids_gate, wl.E, 0.04)
+    L, R, t = _layer(wl, I)
+    c_dev = torch.from_numpy(cached).to(dev())
+    c_out = torch.empty_like(c_dev)
+    unchanged = torch.zeros(1, dtype=torch.int32, device=dev())
+    L.forward_cached(t["x"], t["w1"], t["w3"], t["w2"], cached=c_dev, cache_out=c_out,
+                     unchanged=unchanged, w_g=t["w_g"], bias=t["bias"], renorm=wl.renorm,
+                     capacity=wl.capacity[0], gate_stream=torch.cuda.Stream())
+    torch.cuda.synchronize()
+    ids = _routing_ok(L, logits, wl)
+    assert int(unchanged.item()) == int(O.cache_unchanged(ids, cached).sum())
+    assert int(unchanged.item()) >= 0.95 * wl.T
+    np.testing.assert_array_equal(to_np(c_out), ids)
+    wts = O.gate_weights(O.softmax(logits), cached, wl.renorm)
+    assert_close(to_np(L.cached_weights), wts, 1e-5, "weights at cached picks")
+    counts = O.count_assignments(cached, wl.E)
+    kind, num, den = wl.capacity[0]
+    cap = O.capacity_dynamic(counts, wl.T, num, den)
+    s = O.assign_slots(cached, wl.E, cap, O.exclusive_offsets(cap), R)
+    dest = s["dest_row"]
+    np.testing.assert_array_equal(to_np(L.dest_row), dest)
+    toks = _sample(dest, 32, 5)
+    tt, jj = np.nonzero(dest[toks] >= 0)
+    rows, rtok, e_of = dest[toks][tt, jj], toks[tt], cached[toks][tt, jj]
+    fr = O.ffn_rows_fwd(X[rtok], e_of, LazyF64(I.w1), LazyF64(I.w3), LazyF64(I.w2), wl.act, "bf16")
+    dsub = -np.ones_like(dest[toks])
+    dsub[tt, jj] = np.arange(len(rows))
+    y_ref = O.combine(fr["Y"], dsub, wts[toks], "bf16")
+    assert_close(to_np(L.y)[toks], y_ref, RTOL["bf16"], "y with cached picks")
+
+
+def test_capacity_policy_full_size_counts():
+    wl = W.config("c5")
+    T, E, k, N, delta = wl.T, wl.E, wl.k, 12, 1
+    traj = W.drifting_assignments(wl.seed, T, E, k, N)
+    init = O.capacity_static(T, k, E, 1, 1)
+    pol = B.CapacityPolicy(T, k, E, delta, (21, 20), (5, 4), init)
+    R = rows_alloc_for("dynamic", T, k, E, 21, 20)
+    d = 8
+    x = torch.zeros(T, d, dtype=torch.bfloat16, device=dev())
+    cap = torch.empty(E, dtype=torch.int32, device=dev())
+    off = torch.empty(E + 1, dtype=torch.int32, device=dev())
+    counts = torch.empty(E, dtype=torch.int32, device=dev())
+    fill = torch.empty(E, dtype=torch.int32, device=dev())
+    dest = torch.empty(T, k, dtype=torch.int32, device=dev())
+    src = torch.empty(R, dtype=torch.int32, device=dev())
+    xd = torch.empty(R, d, dtype=torch.bfloat16, device=dev())
+    status = torch.zeros(1, dtype=torch.int32, device=dev())
+    ws = B.workspace(B.moe_dispatch_workspace_bytes(T, E, k), dev())
+    caps, fills = [], torch.empty(N, E, dtype=torch.int32, device=dev())
+    for i in range(N):
+        rows, _ = pol.begin(cap, off)
+        assert rows <= R
+        caps.append(pol.state()["cap"])
+        B.moe_dispatch(x, torch.from_numpy(traj[i]).to(dev()), E, cap, off, R, counts, fill, dest,
+                       src, xd, status, ws)
+        pol.end(counts)
+        fills[i].copy_(fill)
+    torch.cuda.synchronize()
+    pol.close()
+    seq = [O.count_assignments(a, E) for a in traj]
+    sim = O.simulate_capacity_policy(seq, T, k, delta, init, (21, 20), (5, 4))
+    np.testing.assert_array_equal(np.array(caps), sim["caps"])
+    np.testing.assert_array_equal((np.array(seq) - to_np(fills)).sum(axis=1), sim["drops"])
+    assert int(status.item()) == 0
