@@ -105,20 +105,32 @@ template <typename T> struct Raw8 {
 // ---------------------------------------------------------------------------
 // activations (shared by forward epilogue, backward epilogue and transposes)
 // ---------------------------------------------------------------------------
+// The epilogues evaluate these once per output element, so they use the
+// hardware base-2 exponential and reciprocal (relative error about 1e-6,
+// far below the bf16 rounding of the stored results):
+//   e^x = 2^(x log2 e),  sigmoid(h) = 1 / (1 + e^-h),
+//   tanh(u) = 1 - 2 / (1 + e^(2u))  (both limits exact: e^(2u) -> inf or 0).
+__device__ __forceinline__ float exp_fast(float x) {
+  return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
+}
+__device__ __forceinline__ float rcp_fast(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ float tanh_fast(float u) {
+  return 1.f - 2.f * rcp_fast(1.f + exp_fast(2.f * u));
+}
 __device__ __forceinline__ float act_f(float h, int act) {
   if (act == ACT_RELU) return fmaxf(h, 0.f);
   // GELU, tanh form
   const float u = 0.7978845608028654f * (h + 0.044715f * h * h * h);
-  return 0.5f * h * (1.f + tanhf(u));
+  return 0.5f * h * (1.f + tanh_fast(u));
 }
 __device__ __forceinline__ float act_grad_f(float h, int act) {
   if (act == ACT_RELU) return h > 0.f ? 1.f : 0.f;
   const float u = 0.7978845608028654f * (h + 0.044715f * h * h * h);
-  const float th = tanhf(u);
+  const float th = tanh_fast(u);
   const float du = 0.7978845608028654f * (1.f + 3.f * 0.044715f * h * h);
   return 0.5f * (1.f + th) + 0.5f * h * (1.f - th * th) * du;
 }
-__device__ __forceinline__ float sigm(float h) { return 1.f / (1.f + expf(-h)); }
+__device__ __forceinline__ float sigm(float h) { return rcp_fast(1.f + exp_fast(-h)); }
 
 // ---------------------------------------------------------------------------
 // schedule
