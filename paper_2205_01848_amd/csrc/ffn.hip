@@ -793,7 +793,12 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
 // ---------------------------------------------------------------------------
 // split-K reduction
 // ---------------------------------------------------------------------------
-// dW[g] = sum over the expert's split slots, in slot order.
+// dW[g] = sum over the expert's split slots, in slot order.  A bounded grid
+// strides over the elements (blockIdx.y = expert), so experts without a
+// split cost one early exit per block rather than a launch per 1024
+// elements.
+constexpr int kReduceBlocks = 256;   // blocks per expert
+
 __global__ __launch_bounds__(256) void split_reduce_kernel(
     const float* __restrict__ partial, int64_t slot_elems, const Sched* __restrict__ sc,
     float* __restrict__ dwA, float* __restrict__ dwB, int64_t dw_gstride, int split_row,
@@ -801,19 +806,21 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(
   const int g = blockIdx.y;
   const int ns = sc->nsplit[g];
   if (ns <= 1) return;
-  const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
-  if (i >= slot_elems) return;
-  const float* p0 = partial + static_cast<int64_t>(sc->slot0[g]) * slot_elems + i;
-  float4 acc = *reinterpret_cast<const float4*>(p0);
-  for (int s = 1; s < ns; ++s) {
-    const float4 v = *reinterpret_cast<const float4*>(p0 + static_cast<int64_t>(s) * slot_elems);
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  const float* base = partial + static_cast<int64_t>(sc->slot0[g]) * slot_elems;
+  for (int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4; i < slot_elems;
+       i += static_cast<int64_t>(gridDim.x) * 1024) {
+    const float* p0 = base + i;
+    float4 acc = *reinterpret_cast<const float4*>(p0);
+    for (int s = 1; s < ns; ++s) {
+      const float4 v = *reinterpret_cast<const float4*>(p0 + static_cast<int64_t>(s) * slot_elems);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    const int64_t row = i / N, col = i % N;
+    float* dst = row < split_row
+                     ? dwA + static_cast<int64_t>(g) * dw_gstride + row * N + col
+                     : dwB + static_cast<int64_t>(g) * dw_gstride + (row - split_row) * N + col;
+    *reinterpret_cast<float4*>(dst) = acc;
   }
-  const int64_t row = i / N, col = i % N;
-  float* dst = row < split_row
-                   ? dwA + static_cast<int64_t>(g) * dw_gstride + row * N + col
-                   : dwB + static_cast<int64_t>(g) * dw_gstride + (row - split_row) * N + col;
-  *reinterpret_cast<float4*>(dst) = acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -939,7 +946,8 @@ moe_status launch_gemm(hipStream_t s, moe_dtype dt, const GemmParams& p) {
 moe_status launch_split_reduce(hipStream_t s, const FfnPlan& pl, char* ws, int M_out, int N,
                                float* dwA, float* dwB, int split_row) {
   const int64_t elems = static_cast<int64_t>(M_out) * N;
-  dim3 grid(cdiv(elems, 1024), pl.E);
+  const int64_t bx = cdiv(elems, 1024);
+  dim3 grid(static_cast<unsigned>(bx < kReduceBlocks ? bx : kReduceBlocks), pl.E);
   MOE_TIMED("split_reduce", s);
   split_reduce_kernel<<<grid, 256, 0, s>>>(
       reinterpret_cast<const float*>(ws + pl.o_part), elems,
