@@ -54,92 +54,159 @@ __device__ __forceinline__ void finish_token(const float* l, int E, int k,
 
 constexpr int kGateTile = 32;   // tokens per MFMA row tile
 constexpr int kGateWaves = 4;   // waves per workgroup
+constexpr int kGateStage = kGateTile * 128;   // one K step of a tile: 32 rows x 64 bf16
+
+// Buffer resource over a whole operand; an offset of 0x80000000 is out of
+// range (every real offset stays below 2^31, checked on the host), so such a
+// lane reads zeros: ragged token rows, absent experts and K tails.
+constexpr uint32_t kGateOob = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t gate_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           0x7FFFFFFF, 0x00020000);
+}
+
+// LDS of one wave: one K step of the tile's 32 token rows (4 KB), then the
+// step's w_g rows (8 EB rows).  Row q at q * 128 bytes; its 16-byte chunk c
+// at (c ^ ((q >> 1) & 7)).
+template <int EB> struct GateStage {
+  static constexpr int kW = kGateStage;                 // w_g rows start
+  static constexpr int kBytes = kW + EB * 8 * 128;
+};
 
 // A workgroup scores kGateWaves / S token tiles of 32 tokens; the S waves of
-// one tile split K: wave w of the tile takes the 64-wide K steps w, w+S,
-// w+2S, ..., each wave keeping U steps of loads in flight.  S = 1 suits long
-// batches (each wave streams whole rows, U = 1 measured fastest there);
-// small batches take S = 2 or 4 (with U = 2) so the grid still fills the
-// chip.  The S partial scores are summed through LDS in a fixed order.
-template <int NT, int U>  // expert tiles of 32 (E <= 32*NT); K steps per load batch
+// one tile split K: wave w of the tile takes the 64-wide K steps w, w+S, ...
+// (S = 1 on long batches; 2 or 4 so that short batches still fill the chip).
+// Each wave loads a K step of its tile's rows, and the step's rows of w_g,
+// with 16-byte buffer loads in which 8 lanes cover one row's 128 contiguous
+// bytes, so every fetched cache line is used whole by one instruction.  The
+// loads run P steps ahead into a ring of registers; a step's registers go to
+// the wave's LDS buffer (in-order LDS traffic within a wave needs no
+// barrier), from which the MFMA operands are read.  Every step issues the
+// same loads (out-of-range lanes read zeros), so the loop is branch-free and
+// the compiler waits for exactly the step in use.  The S partial scores are
+// summed through LDS in a fixed order.
+template <int NT, int EB, int P>  // expert tiles of 32 (E <= 32*NT); w_g 8-row blocks (E <= 8*EB); steps in flight
 __global__ __launch_bounds__(256) void gate_fwd_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wg,
     const float* __restrict__ bias, int T, int d, int E, int k, int renorm,
     int S, float* __restrict__ logits, int32_t* __restrict__ ids,
     float* __restrict__ weights) {
-  constexpr int P = NT * 32 + 1;  // LDS row pitch (floats)
-  __shared__ float part[kGateWaves][kGateTile][P];
+  using G = GateStage<EB>;
+  constexpr int PITCH = NT * 32 + 1;  // partial-score row pitch (floats)
+  constexpr int NB = 4 + EB;          // 16-byte loads per lane per K step
+  static_assert(kGateTile * PITCH * 4 <= G::kBytes, "partial scores fit in a wave's buffer");
+  __shared__ __attribute__((aligned(16))) char smem[kGateWaves * G::kBytes];
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int lane = threadIdx.x & 63;
   const int r = lane & 31, half = lane >> 5;
   const int tiles = kGateWaves / S;
   const int tile = wave / S, split = wave - tile * S;
   const int t0 = (blockIdx.x * tiles + tile) * kGateTile;
-  int trow = t0 + r;
-  if (trow >= T) trow = T - 1;  // clamp loads; results of such rows are not stored
-  const uint16_t* xr = x + static_cast<size_t>(trow) * d;
-  const uint16_t* wr[NT];
+  const int nsteps = (d + 63) / 64;
+  const int nmy = split < nsteps ? (nsteps - split + S - 1) / S : 0;   // this wave's K steps
+  char* buf = smem + wave * G::kBytes;
+  const __amdgpu_buffer_rsrc_t rx = gate_rsrc(x + static_cast<size_t>(t0) * d);
+  const __amdgpu_buffer_rsrc_t rw = gate_rsrc(wg);
+  // this lane's row within each 8-row block and its chunk, both for the
+  // global read (chunk = 16 contiguous bytes) and the swizzled LDS write
+  const int rowb = lane >> 3, lc = lane & 7;
+  uint32_t roff[NB];      // byte offset of the lane's chunk in step 0, or out of range
+  int wofs[NB];           // LDS byte offset of the lane's chunk
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    int n = nt * 32 + r;
-    wr[nt] = wg + static_cast<size_t>(n < E ? n : 0) * d;
+  for (int blk = 0; blk < NB; ++blk) {
+    const bool is_x = blk < 4;
+    const int row = 8 * (is_x ? blk : blk - 4) + rowb;
+    const bool ok = is_x ? t0 + row < T : row < E;
+    roff[blk] = ok ? static_cast<uint32_t>(row * d * 2 + lc * 16) : kGateOob;
+    wofs[blk] = (is_x ? 0 : G::kW) + row * 128 + ((lc ^ ((row >> 1) & 7)) << 4);
   }
   floatx16 acc[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
     for (int i = 0; i < 16; ++i) acc[nt][i] = 0.f;
 
-  // K mapping shared by both operands: step s, lane half h, MFMA i, element
-  // q carries k = 64 s + 32 h + 8 i + q.
-  const int nsteps = (d + 63) / 64;
-  for (int s0 = split; s0 < nsteps; s0 += S * U) {
-    uint4 av[U][4];
-    uint4 bv[U][NT][4];
+  uint4 ring[P][NB];
+  // K step j of this wave into ring slot u (zeros beyond the wave's steps
+  // or beyond d)
+  auto issue = [&](int j, uint4 (&slot)[NB]) {
+    const int kt = split + j * S;
+    // out of range as arithmetic, not a branch: setting bit 31 of an offset
+    // puts it beyond the buffer (a scalar offset of 2^31 does so for steps
+    // past this wave's last)
+    const uint32_t kbad = static_cast<uint32_t>(kt * 64 + lc * 8 >= d) << 31;
+    const int soff = j < nmy ? kt * 128 : static_cast<int>(kGateOob);
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int blk = 0; blk < NB; ++blk)
+      slot[blk] = __builtin_bit_cast(
+          uint4, __builtin_amdgcn_raw_buffer_load_b128(blk < 4 ? rx : rw, roff[blk] | kbad, soff, 0));
+  };
+  // issue order matters (loads complete in order): keep the compiler from
+  // reordering the prologue's steps
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int kk = (s0 + u * S) * 64 + half * 32 + i * 8;
-        const bool ok = kk < d;
-        av[u][i] = ok ? *reinterpret_cast<const uint4*>(xr + kk) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const bool okb = ok && (nt * 32 + r) < E;
-          bv[u][nt][i] = okb ? *reinterpret_cast<const uint4*>(wr[nt] + kk) : make_uint4(0, 0, 0, 0);
-        }
-      }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bf16x8 a = __builtin_bit_cast(bf16x8, av[u][i]);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          bf16x8 b = __builtin_bit_cast(bf16x8, bv[u][nt][i]);
-          acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[nt], 0, 0, 0);
-        }
-      }
+  for (int u = 0; u < P; ++u) {
+    issue(u, ring[u]);
+    __builtin_amdgcn_sched_barrier(0);
   }
+
+  // K mapping shared by both operands: step kt, MFMA i, lane half h,
+  // element q carries k = 64 kt + 16 i + 8 h + q.
+  const int sw = (r >> 1) & 7;
+  auto step = [&](int j, uint4 (&slot)[NB]) {
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk) *reinterpret_cast<uint4*>(buf + wofs[blk]) = slot[blk];
+    issue(j + P, slot);   // the slot's registers are in LDS: refill it
+    uint4 a[4], b[NT][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = ((2 * i + half) ^ sw) << 4;
+      a[i] = *reinterpret_cast<const uint4*>(buf + r * 128 + c);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        // lanes beyond the loaded w_g rows read a loaded row and use zeros
+        const int n = nt * 32 + r, nr = n & (8 * EB - 1);
+        const uint4 v = *reinterpret_cast<const uint4*>(
+            buf + G::kW + nr * 128 + (((2 * i + half) ^ ((nr >> 1) & 7)) << 4));
+        const uint32_t m = 0u - static_cast<uint32_t>(n < 8 * EB);   // all ones or zero
+        b[nt][i] = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[i]),
+                                                          __builtin_bit_cast(bf16x8, b[nt][i]),
+                                                          acc[nt], 0, 0, 0);
+  };
+  for (int j0 = 0; j0 < nmy; j0 += P) {
+#pragma unroll
+    for (int u = 0; u < P; ++u) step(j0 + u, ring[u]);
+  }
+
+  // the buffers now hold the partial scores
+  __syncthreads();
+  float (*part)[PITCH] = reinterpret_cast<float (*)[PITCH]>(buf);
   // accumulator layout: register q holds row (q/4)*8 + 4*half + q%4, column r
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const int row = (q >> 2) * 8 + half * 4 + (q & 3);
-      part[wave][row][nt * 32 + r] = acc[nt][q];
+      part[row][nt * 32 + r] = acc[nt][q];
     }
   }
   __syncthreads();
+  auto wpart = [&](int w) { return reinterpret_cast<float (*)[PITCH]>(smem + w * G::kBytes); };
   // sum each tile's K partials in split order, add the bias; logits out,
   // coalesced along E
   const int tb = blockIdx.x * tiles * kGateTile;
   for (int idx = threadIdx.x; idx < tiles * kGateTile * E; idx += 256) {
     const int row = idx / E, e = idx - row * E;
     const int tt = row / kGateTile, rr = row - tt * kGateTile;
-    float v = part[tt * S][rr][e];
-    for (int w = 1; w < S; ++w) v += part[tt * S + w][rr][e];
+    float v = wpart(tt * S)[rr][e];
+    for (int w = 1; w < S; ++w) v += wpart(tt * S + w)[rr][e];
     v += bias ? bias[e] : 0.f;
-    part[tt * S][rr][e] = v;
+    wpart(tt * S)[rr][e] = v;
     if (tb + row < T) logits[static_cast<size_t>(tb + row) * E + e] = v;
   }
   __syncthreads();
@@ -147,7 +214,7 @@ __global__ __launch_bounds__(256) void gate_fwd_bf16_kernel(
   if (row < tiles * kGateTile && tb + row < T) {
     const int tt = row / kGateTile, rr = row - tt * kGateTile;
     const size_t t = tb + row;
-    finish_token(&part[tt * S][rr][0], E, k, renorm, ids + t * k, weights + t * k);
+    finish_token(&wpart(tt * S)[rr][0], E, k, renorm, ids + t * k, weights + t * k);
   }
 }
 
@@ -313,24 +380,28 @@ extern "C" moe_status moe_gate_topk(void* stream, moe_dtype dt, int T, int d,
   if (T == 0) return MOE_OK;
   if (!x || !w_g || !logits || !ids || !weights) return MOE_EINVAL;
   if (!aligned16(x) || !aligned16(w_g)) return MOE_EINVAL;
+  // bf16 buffer offsets (a 32-row tile of x, all of w_g) stay below 2^31
+  if (dt == MOE_BF16 && static_cast<int64_t>(d) * 2 * kMaxE >= (int64_t(1) << 31))
+    return MOE_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   MOE_TIMED("gate_fwd", s);
   if (dt == MOE_BF16) {
     const int S = gate_split(T);
     const int tok_per_block = kGateTile * (kGateWaves / S);
     dim3 grid((T + tok_per_block - 1) / tok_per_block);
-    auto go = [&](auto nt, auto u) {
-      gate_fwd_bf16_kernel<decltype(nt)::value, decltype(u)::value><<<grid, 256, 0, s>>>(
-          static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_g), bias, T, d, E,
-          k, renorm, S, logits, ids, weights);
+    auto go = [&](auto nt, auto eb, auto p) {
+      gate_fwd_bf16_kernel<decltype(nt)::value, decltype(eb)::value, decltype(p)::value>
+          <<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(x),
+                                static_cast<const uint16_t*>(w_g), bias, T, d, E, k, renorm, S,
+                                logits, ids, weights);
     };
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
-    if (E <= 32) {
-      if (S == 1) go(I1{}, I1{}); else go(I1{}, I2{});
-    } else {
-      if (S == 1) go(I2{}, I1{}); else go(I2{}, I2{});
-    }
+    using I3 = std::integral_constant<int, 3>;
+    if (E <= 8) go(I1{}, I1{}, I3{});
+    else if (E <= 16) go(I1{}, I2{}, I3{});
+    else if (E <= 32) go(I1{}, std::integral_constant<int, 4>{}, I3{});
+    else go(I2{}, std::integral_constant<int, 8>{}, I2{});
   } else {
     gate_fwd_f32_kernel<<<dim3((T + 63) / 64), 64, 0, s>>>(
         static_cast<const float*>(x), static_cast<const float*>(w_g), bias, T, d,

@@ -341,3 +341,63 @@ def test_capacity_policy_on_device_counts(delta):
     assert st["launched"] == N and st["consumed"] == N - 1 - delta
     assert st["recompiles"] == int(sim["recompile"].sum()) > 0
     assert int(status.item()) == 0
+
+
+# ---- error paths -------------------------------------------------------------------
+def test_policy_call_order_and_state():
+    """begin twice, or end without begin, is rejected without enqueuing; the
+    object stays usable, and destroying it with copies in flight is safe."""
+    T, E, k = 1000, 4, 2
+    pol = B.CapacityPolicy(T, k, E, 2, (11, 10), (3, 2), [500] * E)
+    cap = torch.empty(E, dtype=torch.int32, device=dev())
+    off = torch.empty(E + 1, dtype=torch.int32, device=dev())
+    counts = torch.tensor([400, 600, 500, 500], dtype=torch.int32, device=dev())
+    with pytest.raises(B.MoEError):
+        pol.end(counts)                        # end without begin
+    rows, rec = pol.begin(cap, off)
+    assert rows == 2000 and not rec
+    with pytest.raises(B.MoEError):
+        pol.begin(cap, off)                    # begin twice
+    pol.end(counts)
+    recs = []
+    for _ in range(3):                         # iteration 0's metric is seen by iteration 3
+        recs.append(pol.begin(cap, off)[1])
+        pol.end(counts)
+    torch.cuda.synchronize()
+    assert recs == [False, False, True]
+    st = pol.state()
+    assert st["launched"] == 4 and st["consumed"] == 1 and st["recompiles"] == 1
+    assert st["cap"] == [440, 660, 550, 550]   # ceil(1.1 * counts): 600 overflowed 500
+    np.testing.assert_array_equal(to_np(cap), [440, 660, 550, 550])
+    np.testing.assert_array_equal(to_np(off), [0, 440, 1100, 1650, 2200])
+    rows, rec = pol.begin(cap, off)            # iteration 1's metric fits: no change
+    assert rows == 2200 and not rec
+    pol.end(counts)
+    pol.close()                                # copies still outstanding: waited for
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_loss_kernels_treat_rows_beyond_rows_alloc_as_dropped(dt):
+    rng = np.random.default_rng(77)
+    T, E, k, d = 300, 4, 2, 64
+    ids, dest, R, _ = _routing(rng, T, E, k)
+    bad = dest.copy()
+    bad[::5, 1] = R + 3                        # not a row of y_disp
+    yd = _enc(rng.standard_normal((R, d)), dt)
+    tgt = _enc(rng.standard_normal((T, d)), dt)
+    wts = rng.random((T, k)).astype(np.float32)
+    t_bad = torch.from_numpy(bad.astype(np.int32)).to(dev())
+    agg = torch.full((T * k, d), float("nan"), dtype=torch_dtype(dt), device=dev())
+    B.moe_aggregate_spec(to_dev(yd, dt), t_bad, agg)
+    dyd = torch.full((R, d), float("nan"), dtype=torch_dtype(dt), device=dev())
+    dwt = torch.empty(T, k, dtype=torch.float32, device=dev())
+    loss = torch.empty(1, dtype=torch.float32, device=dev())
+    ws = B.workspace(B.moe_spec_loss_workspace_bytes(T), dev())
+    B.moe_spec_loss(to_dev(yd, dt), t_bad, torch.from_numpy(wts).to(dev()), to_dev(tgt, dt), dyd,
+                    dwt, loss, ws)
+    torch.cuda.synchronize()
+    as_dropped = np.where(bad >= R, -1, bad)
+    np.testing.assert_array_equal(to_np(agg), O.aggregate_spec(_dec(yd, dt), as_dropped))
+    rl, rdw, _ = O.spec_loss(_dec(yd, dt), as_dropped, wts.astype(np.float64), _dec(tgt, dt), dt)
+    assert_close(to_np(loss), np.array([rl]), 1e-5, "loss")
+    assert_close(to_np(dwt), rdw, 1e-5, "dweights")
