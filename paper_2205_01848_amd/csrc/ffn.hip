@@ -440,12 +440,21 @@ __device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0
   constexpr int kWaitVm0 = 0x0F70;    // vmcnt(0)
   constexpr int kWaitLgkm0 = 0xC07F;  // lgkmcnt(0)
   // one ping-pong phase pair: read half h of a stage, then its 16 MFMAs
+  // A wave whose rows or columns of the tile are all beyond the valid ones
+  // (the ragged last tile of an expert, the last column tile) skips its
+  // reads and MFMAs; it still takes part in every barrier.  Its accumulators
+  // stay zero and the epilogue stores none of them.
+  bool active = true;
+  if constexpr (!FULL) {
+    const int wcols = GATED ? 32 : 64;   // the wave's columns (gated: hidden units)
+    active = team * 128 < op.a.rows && wq * wcols < op.b.rows;
+  }
   auto half = [&](const char* sa, const char* sb, int h, bool wait_loads) {
-    fread(sa, sb, h);
+    if (active) fread(sa, sb, h);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    mma();
+    if (active) mma();
     __builtin_amdgcn_sched_barrier(0);
     if (wait_loads) __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __builtin_amdgcn_s_barrier();
