@@ -200,8 +200,8 @@ extern "C" moe_status moe_balance_fwd(void* stream, int T, int E, int k, float l
                                       const float* logits, const int32_t* counts,
                                       float* loss, float* dprob_coef, void* workspace,
                                       size_t workspace_bytes) {
-  // lambda >= 0 and finite (NaN fails the first test, +inf the second)
-  if (!shape_ok(T, E, k) || !(lambda >= 0.f) || !(lambda <= 3.4e38f)) return MOE_EINVAL;
+  // lambda >= 0 and finite (NaN fails the first test)
+  if (!shape_ok(T, E, k) || !(lambda >= 0.f) || !__builtin_isfinite(lambda)) return MOE_EINVAL;
   if (!counts || !loss || !dprob_coef || (T > 0 && !logits)) return MOE_EINVAL;
   const size_t need = moe_balance_workspace_bytes(T, E);
   if (!workspace || workspace_bytes < need) return MOE_EWORKSPACE;

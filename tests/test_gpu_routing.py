@@ -33,6 +33,8 @@ def _run_gate(x_np, wg_np, b_np, k, renorm, dt):
     (517, 128, 64, 1, 0, "bf16"),
     (333, 64, 33, 3, 1, "bf16"),
     (70, 200, 16, 8, 1, "bf16"),
+    (2000, 96, 24, 2, 1, "bf16"),     # 17-32 experts: four 8-row blocks of w_g
+    (301, 72, 32, 3, 0, "bf16"),
     (1, 8, 1, 1, 0, "bf16"),
     # long batches: two waves per token tile, then one (whole rows per wave)
     (40001, 72, 8, 2, 1, "bf16"),
