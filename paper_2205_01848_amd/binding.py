@@ -121,6 +121,32 @@ def _dt(t: torch.Tensor) -> int:
     raise MoEError(f"unsupported layer dtype {t.dtype}")
 
 
+_I32, _F32 = torch.int32, torch.float32
+
+
+def _need(t: Optional[torch.Tensor], n: int, name: str, dtype=None, optional=False):
+    """Refuse a tensor with fewer than the n elements the entry point reads or
+    writes, or of the wrong element type.  The C ABI takes bare pointers and
+    cannot check sizes; an undersized buffer would be accessed past its end."""
+    if t is None:
+        if optional:
+            return
+        raise MoEError(f"{name} is required")
+    if dtype is not None and t.dtype != dtype:
+        raise MoEError(f"{name}: element type {t.dtype}, expected {dtype}")
+    if t.numel() < n:
+        raise MoEError(f"{name} holds {t.numel()} elements, the call needs {n}")
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
+def _planes(act: int) -> int:
+    """[rows_alloc, f] planes of h_save: H, A; or H1, H3, A for SwiGLU."""
+    return 3 if act == MOE_SWIGLU else 2
+
+
 def workspace(nbytes: int, device) -> torch.Tensor:
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
@@ -129,6 +155,11 @@ def workspace(nbytes: int, device) -> torch.Tensor:
 def moe_gate_topk(x, w_g, bias, k, renorm, logits, ids, weights):
     T, d = x.shape
     E = w_g.shape[0]
+    _need(w_g, E * d, "w_g", x.dtype)
+    _need(bias, E, "bias", _F32, optional=True)
+    _need(logits, T * E, "logits", _F32)
+    _need(ids, T * k, "ids", _I32)
+    _need(weights, T * k, "weights", _F32)
     _check(lib().moe_gate_topk(_stream(), _dt(x), T, d, E, k, int(renorm), _ptr(x), _ptr(w_g),
                                _ptr(bias), _ptr(logits), _ptr(ids), _ptr(weights)),
            "moe_gate_topk")
@@ -136,11 +167,17 @@ def moe_gate_topk(x, w_g, bias, k, renorm, logits, ids, weights):
 
 def moe_count(ids, E, counts, status):
     T, k = ids.shape
+    _need(ids, T * k, "ids", _I32)
+    _need(counts, E, "counts", _I32)
+    _need(status, 1, "status", _I32)
     _check(lib().moe_count(_stream(), T, E, k, _ptr(ids), _ptr(counts), _ptr(status)),
            "moe_count")
 
 
 def moe_update_capacity(T, k, E, counts, num, den, cap_min, capacity, offsets):
+    _need(counts, E, "counts", _I32, optional=True)
+    _need(capacity, E, "capacity", _I32)
+    _need(offsets, E + 1, "offsets", _I32)
     _check(lib().moe_update_capacity(_stream(), T, k, E, _ptr(counts), num, den, cap_min,
                                      _ptr(capacity), _ptr(offsets)), "moe_update_capacity")
 
@@ -153,10 +190,16 @@ def moe_dispatch(x, ids, E, capacity, offsets, rows_alloc, counts, fill, dest_ro
                  status, ws):
     T, d = x.shape
     k = ids.shape[1]
+    _need(ids, T * k, "ids", _I32)
+    for t, n, name in ((capacity, E, "capacity"), (offsets, E + 1, "offsets"),
+                       (counts, E, "counts"), (fill, E, "fill"), (dest_row, T * k, "dest_row"),
+                       (src, rows_alloc, "src"), (status, 1, "status")):
+        _need(t, n, name, _I32)
+    _need(x_disp, rows_alloc * d, "x_disp", x.dtype)
     _check(lib().moe_dispatch(_stream(), _dt(x), T, d, E, k, _ptr(x), _ptr(ids), _ptr(capacity),
                               _ptr(offsets), rows_alloc, _ptr(counts), _ptr(fill),
                               _ptr(dest_row), _ptr(src), _ptr(x_disp), _ptr(status), _ptr(ws),
-                              ws.numel()), "moe_dispatch")
+                              _nbytes(ws)), "moe_dispatch")
 
 
 def moe_ffn_fwd_workspace_bytes(dt, act, E, d, f, rows_alloc) -> int:
@@ -169,15 +212,27 @@ def moe_ffn_bwd_workspace_bytes(dt, act, E, d, f, rows_alloc) -> int:
 
 def moe_expert_ffn_fwd(act, offsets, rows, x_disp, w1, w3, w2, h_save, y_disp, ws):
     E, f, d = w1.shape
+    R, dt = x_disp.shape[0], w1.dtype
+    _need(offsets, E + 1, "offsets", _I32)
+    _need(rows, E, "rows", _I32)
+    _need(x_disp, R * d, "x_disp", dt)
+    _need(w3, E * f * d, "w3", dt, optional=act != MOE_SWIGLU)
+    _need(w2, E * d * f, "w2", dt)
+    _need(h_save, _planes(act) * R * f, "h_save", dt, optional=True)
+    _need(y_disp, R * d, "y_disp", dt)
     _check(lib().moe_expert_ffn_fwd(_stream(), _dt(w1), act, E, d, f, _ptr(offsets), _ptr(rows),
                                     x_disp.shape[0], _ptr(x_disp), _ptr(w1), _ptr(w3), _ptr(w2),
-                                    _ptr(h_save), _ptr(y_disp), _ptr(ws), ws.numel()),
+                                    _ptr(h_save), _ptr(y_disp), _ptr(ws), _nbytes(ws)),
            "moe_expert_ffn_fwd")
 
 
 def moe_combine(y_disp, dest_row, weights, y):
     T, k = dest_row.shape
     d = y.shape[1]
+    _need(y_disp, y_disp.shape[0] * d, "y_disp", y.dtype)
+    _need(dest_row, T * k, "dest_row", _I32)
+    _need(weights, T * k, "weights", _F32)
+    _need(y, T * d, "y")
     _check(lib().moe_combine(_stream(), _dt(y), T, d, k, y_disp.shape[0], _ptr(y_disp),
                              _ptr(dest_row), _ptr(weights), _ptr(y)), "moe_combine")
 
@@ -185,6 +240,13 @@ def moe_combine(y_disp, dest_row, weights, y):
 def moe_combine_bwd(dy, y_disp, dest_row, weights, dy_disp, dweights):
     T, k = dest_row.shape
     d = dy.shape[1]
+    R = y_disp.shape[0]
+    _need(dy, T * d, "dy")
+    _need(y_disp, R * d, "y_disp", dy.dtype)
+    _need(dest_row, T * k, "dest_row", _I32)
+    _need(weights, T * k, "weights", _F32)
+    _need(dy_disp, R * d, "dy_disp", dy.dtype)
+    _need(dweights, T * k, "dweights", _F32)
     _check(lib().moe_combine_bwd(_stream(), _dt(dy), T, d, k, y_disp.shape[0], _ptr(dy),
                                  _ptr(y_disp), _ptr(dest_row), _ptr(weights), _ptr(dy_disp),
                                  _ptr(dweights)), "moe_combine_bwd")
@@ -193,10 +255,22 @@ def moe_combine_bwd(dy, y_disp, dest_row, weights, dy_disp, dweights):
 def moe_expert_ffn_bwd(act, offsets, rows, x_disp, h_save, w1, w3, w2, dy_disp, dx_disp, dw1,
                        dw3, dw2, ws):
     E, f, d = w1.shape
+    R, dt, sw = x_disp.shape[0], w1.dtype, act == MOE_SWIGLU
+    _need(offsets, E + 1, "offsets", _I32)
+    _need(rows, E, "rows", _I32)
+    _need(x_disp, R * d, "x_disp", dt)
+    _need(h_save, _planes(act) * R * f, "h_save", dt)
+    _need(w3, E * f * d, "w3", dt, optional=not sw)
+    _need(w2, E * d * f, "w2", dt)
+    _need(dy_disp, R * d, "dy_disp", dt)
+    _need(dx_disp, R * d, "dx_disp", dt)
+    _need(dw1, E * f * d, "dw1", _F32)
+    _need(dw3, E * f * d, "dw3", _F32, optional=not sw)
+    _need(dw2, E * d * f, "dw2", _F32)
     _check(lib().moe_expert_ffn_bwd(_stream(), _dt(w1), act, E, d, f, _ptr(offsets), _ptr(rows),
                                     x_disp.shape[0], _ptr(x_disp), _ptr(h_save), _ptr(w1),
                                     _ptr(w3), _ptr(w2), _ptr(dy_disp), _ptr(dx_disp), _ptr(dw1),
-                                    _ptr(dw3), _ptr(dw2), _ptr(ws), ws.numel()),
+                                    _ptr(dw3), _ptr(dw2), _ptr(ws), _nbytes(ws)),
            "moe_expert_ffn_bwd")
 
 
@@ -208,14 +282,25 @@ def moe_gate_bwd(x, logits, ids, dweights, renorm, dlogits, dw_g, ws, dprob_coef
     T, d = x.shape
     E = logits.shape[1]
     k = ids.shape[1]
+    _need(logits, T * E, "logits", _F32)
+    _need(ids, T * k, "ids", _I32)
+    _need(dweights, T * k, "dweights", _F32)
+    _need(dprob_coef, E, "dprob_coef", _F32, optional=True)
+    _need(dlogits, T * E, "dlogits", _F32)
+    _need(dw_g, E * d, "dw_g", _F32)
     _check(lib().moe_gate_bwd(_stream(), _dt(x), T, d, E, k, int(renorm), _ptr(x), _ptr(logits),
                               _ptr(ids), _ptr(dweights), _ptr(dprob_coef), _ptr(dlogits),
-                              _ptr(dw_g), _ptr(ws), ws.numel()), "moe_gate_bwd")
+                              _ptr(dw_g), _ptr(ws), _nbytes(ws)), "moe_gate_bwd")
 
 
 def moe_dispatch_bwd(dx_disp, dest_row, E, dlogits, w_g, dx):
     T, k = dest_row.shape
     d = dx.shape[1]
+    _need(dx_disp, dx_disp.shape[0] * d, "dx_disp", dx.dtype)
+    _need(dest_row, T * k, "dest_row", _I32)
+    _need(dlogits, T * E, "dlogits", _F32, optional=True)
+    _need(w_g, E * d, "w_g", dx.dtype, optional=True)
+    _need(dx, T * d, "dx")
     _check(lib().moe_dispatch_bwd(_stream(), _dt(dx), T, d, E, k, dx_disp.shape[0],
                                   _ptr(dx_disp), _ptr(dest_row), _ptr(dlogits), _ptr(w_g),
                                   _ptr(dx)), "moe_dispatch_bwd")
@@ -228,14 +313,21 @@ def moe_balance_workspace_bytes(T, E) -> int:
 
 def moe_balance_fwd(logits, counts, k, lam, loss, dprob_coef, ws):
     T, E = logits.shape
+    _need(logits, T * E, "logits", _F32)
+    _need(counts, E, "counts", _I32)
+    _need(loss, 1, "loss", _F32)
+    _need(dprob_coef, E, "dprob_coef", _F32)
     _check(lib().moe_balance_fwd(_stream(), T, E, k, float(lam), _ptr(logits), _ptr(counts),
-                                 _ptr(loss), _ptr(dprob_coef), _ptr(ws), ws.numel()),
+                                 _ptr(loss), _ptr(dprob_coef), _ptr(ws), _nbytes(ws)),
            "moe_balance_fwd")
 
 
 def moe_aggregate_spec(y_disp, dest_row, out):
     T, k = dest_row.shape
     d = out.shape[1]
+    _need(y_disp, y_disp.shape[0] * d, "y_disp", out.dtype)
+    _need(dest_row, T * k, "dest_row", _I32)
+    _need(out, T * k * d, "out")
     _check(lib().moe_aggregate_spec(_stream(), _dt(out), T, d, k, _ptr(y_disp), _ptr(dest_row),
                                     y_disp.shape[0], _ptr(out)), "moe_aggregate_spec")
 
@@ -247,15 +339,26 @@ def moe_spec_loss_workspace_bytes(T) -> int:
 def moe_spec_loss(y_disp, dest_row, weights, target, dy_disp, dweights, loss, ws):
     T, k = dest_row.shape
     d = target.shape[1]
+    R = y_disp.shape[0]
+    _need(y_disp, R * d, "y_disp", target.dtype)
+    _need(dest_row, T * k, "dest_row", _I32)
+    _need(weights, T * k, "weights", _F32)
+    _need(target, T * d, "target")
+    _need(dy_disp, R * d, "dy_disp", target.dtype)
+    _need(dweights, T * k, "dweights", _F32)
+    _need(loss, 1, "loss", _F32)
     _check(lib().moe_spec_loss(_stream(), _dt(target), T, d, k, _ptr(y_disp), _ptr(dest_row),
                                _ptr(weights), _ptr(target), y_disp.shape[0], _ptr(dy_disp),
-                               _ptr(dweights), _ptr(loss), _ptr(ws), ws.numel()),
+                               _ptr(dweights), _ptr(loss), _ptr(ws), _nbytes(ws)),
            "moe_spec_loss")
 
 
 # ---- sample assignment caching ------------------------------------------------
 def moe_cache_update(fresh_ids, cached, cache_out, unchanged):
     T, k = fresh_ids.shape
+    for t, name in ((fresh_ids, "fresh_ids"), (cached, "cached"), (cache_out, "cache_out")):
+        _need(t, T * k, name, _I32)
+    _need(unchanged, 1, "unchanged", _I32)
     _check(lib().moe_cache_update(_stream(), T, k, _ptr(fresh_ids), _ptr(cached), _ptr(cache_out),
                                   _ptr(unchanged)), "moe_cache_update")
 
@@ -263,6 +366,9 @@ def moe_cache_update(fresh_ids, cached, cache_out, unchanged):
 def moe_cached_weights(logits, ids, renorm, weights):
     T, E = logits.shape
     k = ids.shape[1]
+    _need(logits, T * E, "logits", _F32)
+    _need(ids, T * k, "ids", _I32)
+    _need(weights, T * k, "weights", _F32)
     _check(lib().moe_cached_weights(_stream(), T, E, k, int(renorm), _ptr(logits), _ptr(ids),
                                     _ptr(weights)), "moe_cached_weights")
 
@@ -302,6 +408,8 @@ class CapacityPolicy:
     def begin(self, capacity, offsets):
         """Enqueue the capacities for the next launch; returns (rows needed,
         whether the trigger recompiled)."""
+        _need(capacity, self.E, "capacity", _I32)
+        _need(offsets, self.E + 1, "offsets", _I32)
         rows = ctypes.c_int64()
         rec = ctypes.c_int()
         _check(lib().moe_policy_begin(self._h, _stream(), _ptr(capacity), _ptr(offsets),
@@ -309,6 +417,7 @@ class CapacityPolicy:
         return rows.value, bool(rec.value)
 
     def end(self, counts):
+        _need(counts, self.E, "counts", _I32)
         _check(lib().moe_policy_end(self._h, _stream(), _ptr(counts)), "moe_policy_end")
 
     def state(self):

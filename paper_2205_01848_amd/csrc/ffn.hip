@@ -3,11 +3,15 @@
 //
 // Every product is one persistent grouped GEMM kernel in "NT" form,
 //     C[m, n] = sum_k A[m, k] * B[n, k]     (both operands K-contiguous),
-// 256x256 output tiles, K tiles of 128 bytes, 8 wavefronts of 128x64 each
-// on v_mfma_f32_32x32x16_bf16 (fp32 layers: v_mfma_f32_32x32x2f32) in two
-// ping-pong teams (one team's MFMAs overlap the other's LDS reads), operand
-// tiles loaded HBM -> LDS by buffer loads, double-buffered, with an XOR
-// swizzle that keeps the MFMA fragment reads bank-conflict free.
+// 256x256 output tiles, K tiles of 128 bytes, operand tiles loaded HBM ->
+// LDS by buffer loads, double-buffered, with an XOR swizzle that keeps the
+// MFMA fragment reads bank-conflict free.
+//  * bf16 layers: 4 wavefronts of 128x128 on v_mfma_f32_16x16x32_bf16, one
+//    barrier per K step, loads and fragment reads issued one at a time
+//    between the MFMAs (ffn_gemm16_kernel).
+//  * fp32 layers: 8 wavefronts of 128x64 on v_mfma_f32_32x32x2f32 in two
+//    ping-pong teams, one team's MFMAs overlapping the other's LDS reads
+//    (ffn_gemm_kernel).
 //  * var-M products (forward H, Y; backward dA, dX): the M dimension of
 //    expert e is its row count, read on the device; tiles are listed by a
 //    one-workgroup schedule kernel, so no host synchronisation is needed.
@@ -800,6 +804,475 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
 }
 
 // ---------------------------------------------------------------------------
+// bf16 products: four wavefronts of 128x128
+// ---------------------------------------------------------------------------
+// bf16 layers run every product on 4 wavefronts, one per SIMD, each holding a
+// 128x128 block of the 256x256 tile as 64 blocks of 16x16 fp32 accumulators
+// (v_mfma_f32_16x16x32_bf16, 256 accumulation registers).  Per K step of 64
+// there is one barrier.  Between the MFMAs each wave issues, one at a time,
+// the fragment reads of the next half step and, after the barrier, its share
+// of the direct-to-LDS loads of the step after next, so the memory pipeline
+// sees a steady stream of requests while the matrix core stays busy.  A
+// 128x128 block reads a third less LDS per MFMA than a 128x64 one.
+constexpr int kThreads16 = 256;
+constexpr int kP16 = 132;                      // floats per staged row (128 + 4)
+constexpr int kStrip16Bytes = 16 * kP16 * 4;   // 16 rows: two strips per 32 KB array
+
+typedef int intx4 __attribute__((ext_vector_type(4)));
+
+// c += a * b for one 16x16 block.  Lane l = 16 G + c16 supplies row c16 of
+// the A and B sub-blocks at k = 8 G .. 8 G + 7 and holds rows 4 G .. 4 G + 3,
+// column c16 of the result.  Inline assembly keeps each accumulator in place
+// in its accumulation registers through the K loop (compiled MFMAs get their
+// accumulators shuffled between loop iterations).  Consecutive updates of one
+// accumulator are at least 63 MFMAs apart, and the fragments an MFMA reads
+// are not rewritten for at least 28 MFMAs, so no wait states are needed
+// inside the loop; the epilogue waits before it reads the accumulators.
+__device__ __forceinline__ void mfma16(floatx4& c, const uint4& a, const uint4& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+               : "+a"(c)
+               : "v"(__builtin_bit_cast(intx4, a)), "v"(__builtin_bit_cast(intx4, b)));
+}
+
+// acc += A_tile * B_tile^T over the whole K extent (see above).  Wave w owns
+// tile rows 128 (w >> 1) .. +127 and columns 128 (w & 1) .. +127 (gated
+// forward: hidden units 64 (w & 1) .. +63 of W1, then the same units of W3).
+// The four stage objects are distinct, and the loop is unrolled by two so
+// every LDS access names its object statically: the compiler can then tell
+// the loads into one stage from the reads of the other.
+template <int ALAY, int BLAY, bool GATED, bool FULL>
+__device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* lb0, char* la1,
+                                           char* lb1, floatx4 (&acc)[8][8]) {
+  constexpr int KSTEP = 64;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int K = op.K;
+  const int nk = (K + KSTEP - 1) / KSTEP;
+  if (nk <= 0) return;
+  const int nk2 = (nk + 1) & ~1;   // odd counts load one all-zero step
+
+  // ---- loads: 1 KB blocks, as in the 8-wave kernel; wave w loads blocks
+  // 8w .. 8w+7 of A (g = 0..7) and of B (g = 8..15) of every stage.
+  const int l3 = lane >> 3;
+  const int co0 = ((lane & 7) ^ swz(l3)) * 16, co1 = ((lane & 7) ^ swz(l3 + 8)) * 16;
+  const int kr = lane >> 5;            // KM: k-row within the block
+  const int pe = (lane & 31) * 8;      // KM: physical element within the k-row
+  auto km_col = [&](int q) { return (((pe >> 5) ^ q) << 5) + (pe & 31); };
+  const __amdgpu_buffer_rsrc_t ra_t = tile_rsrc(op.a.base);
+  const __amdgpu_buffer_rsrc_t rb_t = tile_rsrc(op.b.base);
+  const __amdgpu_buffer_rsrc_t rb3_t = tile_rsrc(GATED ? op.b.base2 : op.b.base);
+  auto km_rsrc = [&](const Operand& o, int kt, bool second) {
+    const int64_t k = static_cast<int64_t>(kt) * KSTEP - (second ? o.split : 0);
+    return tile_rsrc((second ? o.base2 : o.base) + k * o.ld);
+  };
+  // the resources and flags of one K step, set once per step
+  struct StepLd {
+    __amdgpu_buffer_rsrc_t ra, ra2, rb, rb2;
+    int kt;
+    bool kfull, kany;
+  };
+  auto step_ld = [&](int kt) {
+    StepLd s;
+    s.kt = kt;
+    s.kfull = (kt + 1) * KSTEP <= K;
+    s.kany = kt * KSTEP < K;
+    s.ra = ra_t; s.ra2 = ra_t; s.rb = rb_t; s.rb2 = rb3_t;
+    if constexpr (ALAY == L_KM) {
+      s.ra = km_rsrc(op.a, kt, false);
+      s.ra2 = op.a.base2 ? km_rsrc(op.a, kt, true) : s.ra;
+    }
+    if constexpr (BLAY == L_KM) {
+      s.rb = km_rsrc(op.b, kt, false);
+      s.rb2 = op.b.base2 ? km_rsrc(op.b, kt, true) : s.rb;
+    }
+    return s;
+  };
+  // block blk of operand o (layout LAY) of step s.kt into dst
+  auto load_blk = [&](auto lay, const Operand& o, const __amdgpu_buffer_rsrc_t& rs,
+                      const __amdgpu_buffer_rsrc_t& rs2, char* dst, int blk, const StepLd& s,
+                      bool gated) {
+    constexpr int LAY = decltype(lay)::value;
+    const int ld = static_cast<int>(o.ld);
+    uint32_t off;
+    int soff;
+    bool second = false;
+    if constexpr (LAY == L_KC) {
+      const int co = (blk & 1) ? co1 : co0;
+      // gated forward: 64-row groups alternate W1 / W3 rows of 64 hidden units
+      const int row0 = gated ? (blk >> 4) * 64 + (blk & 7) * 8 : blk * 8;
+      second = gated && ((blk >> 3) & 1);
+      off = static_cast<uint32_t>(l3 * ld) + co;
+      soff = row0 * ld + s.kt * kRowBytes;
+      if (!FULL || !s.kfull) {
+        const bool ok = (FULL || row0 + l3 < o.rows) && (s.kfull || s.kt * kRowBytes + co < K * 2);
+        if (!ok) off = kOob;
+      }
+    } else {
+      const int krel = 2 * blk;                  // first k-row of the block in the step
+      const int kabs = s.kt * KSTEP + krel;
+      const int q = (krel + kr) & 3;
+      const int col = km_col(q);
+      second = kabs >= o.split;
+      off = static_cast<uint32_t>(kr * ld + col * 2);
+      soff = krel * ld;
+      if (!FULL || !s.kfull) {
+        const bool ok = (FULL || col < o.rows) && (s.kfull || kabs + kr < K);
+        if (!ok) off = kOob;
+      }
+    }
+    if (!s.kany) off = kOob;
+    if (second)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs2, MOE_LDS(dst + blk * 1024), 16, off, soff, 0, 0);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, MOE_LDS(dst + blk * 1024), 16, off, soff, 0, 0);
+  };
+  using KC_ = std::integral_constant<int, L_KC>;
+  using KM_ = std::integral_constant<int, L_KM>;
+  // one of the wave's 16 loads of a stage
+  auto load1 = [&](const StepLd& s, char* sa, char* sb, int g) {
+    const int blk = wave * 8 + (g & 7);
+    if (g < 8) {
+      if constexpr (ALAY == L_KC) load_blk(KC_{}, op.a, s.ra, s.ra2, sa, blk, s, false);
+      else load_blk(KM_{}, op.a, s.ra, s.ra2, sa, blk, s, false);
+    } else {
+      if constexpr (BLAY == L_KC) load_blk(KC_{}, op.b, s.rb, s.rb2, sb, blk, s, GATED);
+      else load_blk(KM_{}, op.b, s.rb, s.rb2, sb, blk, s, false);
+    }
+  };
+
+  // ---- fragments.  KC: lane l = 16 G + c16 reads row c16 of a 16-row block,
+  // logical chunk 4h + G (k = 32h + 8G .. +7) of the 128-byte row; the row's
+  // swizzle is (c16 >> 1) since blocks start at multiples of 16.
+  const int c16 = lane & 15, G = lane >> 4;
+  const int fa_kc = (wm * 128 + c16) * kRowBytes, fb_kc = (wn * 128 + c16) * kRowBytes;
+  // KM: two transpose reads, k-rows 32h + 8G + (c16 >> 2) and 4 below, columns
+  // cb + 4 (c16 & 3) .. +3 (lane 4a + b of a 16-lane group then holds column
+  // cb + 4a + b at 4 consecutive k); segment swizzle by k & 3 = c16 >> 2
+  auto km_frag = [&](const char* st, int cb, int h) -> uint4 {
+    const int phys = (((cb >> 5) ^ (c16 >> 2)) << 5) + (cb & 31) + 4 * (c16 & 3);
+    const char* p0 = st + (32 * h + 8 * G + (c16 >> 2)) * 512 + phys * 2;
+    const uint2 lo = read_tr(p0);
+    const uint2 hi = read_tr(p0 + 4 * 512);
+    return make_uint4(lo.x, lo.y, hi.x, hi.y);
+  };
+  // fragment g of half h: A sub-block g (g < 8) or B sub-block g - 8
+  auto read1 = [&](const char* sa, const char* sb, int h, uint4 (&fa)[8], uint4 (&fb)[8], int g) {
+    const int sw = ((4 * h + G) ^ (c16 >> 1)) << 4;
+    if (g < 8) {
+      if constexpr (ALAY == L_KC)
+        fa[g] = *reinterpret_cast<const uint4*>(sa + fa_kc + g * 16 * kRowBytes + sw);
+      else
+        fa[g] = km_frag(sa, wm * 128 + g * 16, h);
+    } else {
+      if constexpr (BLAY == L_KC)
+        fb[g - 8] = *reinterpret_cast<const uint4*>(sb + fb_kc + (g - 8) * 16 * kRowBytes + sw);
+      else
+        fb[g - 8] = km_frag(sb, wn * 128 + (g - 8) * 16, h);
+    }
+  };
+  uint4 f0a[8], f0b[8], f1a[8], f1b[8];   // fragments of k-half 0 / 1 of a stage
+
+  // A wave whose rows or columns of the tile are all beyond the valid ones
+  // skips its reads and MFMAs (it still loads and takes every barrier).
+  bool active = true;
+  if constexpr (!FULL) active = wm * 128 < op.a.rows && wn * (GATED ? 64 : 128) < op.b.rows;
+
+  constexpr int kPre = 8;   // MFMAs of the second half before the barrier
+  // One K step from stage (ca, cb), the next stage in (na, nb); loads of step
+  // kt + 2 go into (ca, cb) once every wave has finished reading it.
+  auto step = [&](int kt, char* ca, char* cb, const char* na, const char* nb) {
+    // first half: MFMAs of k-half 0, one read of k-half 1 per 4 MFMAs
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      if (active) {
+        read1(ca, cb, 1, f1a, f1b, g);
+#pragma unroll
+        for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f0a[m >> 3], f0b[m & 7]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // second half: kPre MFMAs, then wait for stage kt+1 and for every wave's
+    // reads of stage kt; then this wave's loads of step kt+2, the reads of
+    // the next stage's k-half 0 and the remaining MFMAs, interleaved
+    const StepLd s = step_ld(kt + 2);
+    if (active) {
+#pragma unroll
+      for (int m = 0; m < kPre; ++m) mfma16(acc[m >> 3][m & 7], f1a[m >> 3], f1b[m & 7]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    constexpr int kRest = 64 - kPre;
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      load1(s, ca, cb, g);
+      if (active) {
+        read1(na, nb, 0, f0a, f0b, g);
+#pragma unroll
+        for (int m = kPre + kRest * g / 16; m < kPre + kRest * (g + 1) / 16; ++m)
+          mfma16(acc[m >> 3][m & 7], f1a[m >> 3], f1b[m & 7]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  {
+    const StepLd s0 = step_ld(0), s1 = step_ld(1);
+#pragma unroll
+    for (int g = 0; g < 16; ++g) load1(s0, la0, lb0, g);
+#pragma unroll
+    for (int g = 0; g < 16; ++g) load1(s1, la1, lb1, g);
+  }
+  __builtin_amdgcn_s_waitcnt(0x4F70);   // vmcnt(16): this wave's stage-0 loads landed
+  __builtin_amdgcn_s_barrier();
+  if (active) {
+#pragma unroll
+    for (int g = 0; g < 16; ++g) read1(la0, lb0, 0, f0a, f0b, g);
+  }
+  for (int kt = 0; kt < nk2; kt += 2) {
+    step(kt, la0, lb0, la1, lb1);
+    step(kt + 1, la1, lb1, la0, lb0);
+  }
+  __builtin_amdgcn_s_waitcnt(0x0070);
+  __builtin_amdgcn_s_barrier();   // every load landed, every read done: stages are free
+  // the epilogue reads the accumulators with ordinary instructions
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
+
+// Stage rows 16i .. 16i+15 of the wave's accumulators as fp32, row pitch kP16.
+__device__ __forceinline__ void stage16(float* strip, const floatx4 (&acc)[8][8], int i,
+                                        int lane) {
+  const int c16 = lane & 15, G = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) strip[(4 * G + q) * kP16 + 16 * j + c16] = acc[i][j][q];
+}
+
+template <int MODE, int PASS>
+__global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmParams p) {
+  __shared__ __attribute__((aligned(16))) char la0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) char lb0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) char la1[kTileBytes];
+  __shared__ __attribute__((aligned(16))) char lb1[kTileBytes];
+  using T = uint16_t;
+  constexpr int ES = 2;
+  constexpr bool VARK = MODE == M_DW;
+  constexpr bool GATED = MODE == M_FWD1_SWIGLU;
+  constexpr int ALAY = a_layout(PASS), BLAY = b_layout(PASS);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const Sched& sc = *p.sched;
+  const int n_items = VARK ? sc.n_segs * p.mtiles_out * p.ntiles : sc.n_mtiles * p.ntiles;
+  const int G = gridDim.x;
+  const int lbase = (blockIdx.x % kXcds) * (G / kXcds) + blockIdx.x / kXcds;
+
+  for (int round = 0;; ++round) {
+    const int L = round * G + lbase;
+    if (L >= n_items) break;
+    TileOps op;
+    int g, row0, m_valid, n0;
+    int slot = -1, mt, nt;
+    if constexpr (!VARK) {
+      int mti;
+      decode_grouped(L, sc.n_mtiles, p.ntiles, mti, nt);
+      const int2 tm = p.mtile[mti];
+      g = tm.x;
+      row0 = p.offsets[g] + tm.y;
+      m_valid = min(BM, sc.rows[g] - tm.y);
+      op.a = {p.A + static_cast<int64_t>(row0) * p.lda, nullptr, p.lda, m_valid, 0};
+      op.K = p.K;
+      const char* bg = p.B + static_cast<int64_t>(g) * p.b_gstride;
+      if constexpr (GATED) {
+        n0 = nt * (BN / 2);
+        op.b = {bg + static_cast<int64_t>(n0) * p.ldb,
+                p.B2 + static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0) * p.ldb,
+                p.ldb, min(BN / 2, p.N - n0), 0};
+      } else if constexpr (BLAY == L_KC) {
+        n0 = nt * BN;
+        op.b = {bg + static_cast<int64_t>(n0) * p.ldb, nullptr, p.ldb, min(BN, p.N - n0), 0};
+      } else {
+        n0 = nt * BN;
+        op.b = {bg + static_cast<int64_t>(n0) * ES,
+                p.B2 ? p.B2 + static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0) * ES
+                     : nullptr,
+                p.ldb, min(BN, p.N - n0), p.B2 ? p.kmsplit : 0x7FFFFFFF};
+      }
+    } else {
+      const int tmn = p.mtiles_out * p.ntiles;
+      const int si = L / tmn;
+      decode_grouped(L - si * tmn, p.mtiles_out, p.ntiles, mt, nt);
+      const int4 sg = p.seg[si];
+      g = sg.x;
+      slot = sg.w;
+      const int k1 = min(sg.z, sc.rows[g]);
+      const int64_t krow = static_cast<int64_t>(p.offsets[g]) + sg.y;
+      row0 = mt * BM;
+      n0 = nt * BN;
+      m_valid = min(BM, p.M_out - row0);
+      op.a = {p.A + krow * p.lda + static_cast<int64_t>(row0) * ES, nullptr, p.lda, m_valid,
+              0x7FFFFFFF};
+      op.b = {p.B + krow * p.ldb + static_cast<int64_t>(n0) * ES, nullptr, p.ldb,
+              min(BN, p.N - n0), 0x7FFFFFFF};
+      op.K = max(0, k1 - sg.y);
+    }
+
+    floatx4 acc[8][8];
+    if (op.a.rows >= BM && op.b.rows >= (GATED ? BN / 2 : BN))
+      mainloop16<ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc);
+    else
+      mainloop16<ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc);
+
+    // Epilogue, wave by wave: 16 accumulator rows at a time go through the
+    // wave's LDS strip; a lane then finishes 8 consecutive columns of a row
+    // and writes them as one vector (bf16) or two (fp32 weight gradients).
+    // The lane index and the strip address are derived from an opaque zero
+    // produced here, so nothing the epilogue computes per lane is hoisted
+    // and held in registers across the K loop.
+    int z;
+    asm volatile("s_mov_b32 %0, 0" : "=s"(z));
+    const int el = lane + z;
+    float* strip = reinterpret_cast<float*>((wave < 2 ? la0 : lb0) + (wave & 1) * kStrip16Bytes + z);
+    const int wr0 = wm * 128;                     // the wave's first tile row
+    if constexpr (MODE == M_FWD1_SWIGLU) {
+      // strip columns [0,64): H1, [64,128): H3 of hidden units n0 + 64 wn + u
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        stage16(strip, acc, i, el);
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+          const int r = it * 8 + (el >> 3), u8 = (el & 7) * 8;
+          const int lm = wr0 + 16 * i + r;
+          const int gc = n0 + wn * 64 + u8;
+          if (lm < m_valid && gc < p.N) {
+            float h1[8], h3[8], a[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              h1[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kP16 + u8 + e]));
+              h3[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kP16 + 64 + u8 + e]));
+              a[e] = h1[e] * sigm(h1[e]) * h3[e];
+            }
+            const int64_t grow = row0 + lm;
+            if (p.H1) {
+              store_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h1);
+              store_vec<T>(p.H3 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h3);
+            }
+            store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, a);
+          }
+        }
+      }
+    } else if constexpr (MODE == M_BWD_DA || MODE == M_BWD_DA_SWIGLU) {
+      // dH = dA act'(H): 32 (row block, row group) iterations, each reading 8
+      // saved pre-activations (two planes for SwiGLU) per lane, issued kPf
+      // iterations ahead of their use into a ring of kPf + 1 registers
+      constexpr bool SW = MODE == M_BWD_DA_SWIGLU;
+      constexpr int kIt = 32, kPf = 4, kRing = kPf + 1;
+      Raw8<T> q1[kRing], q3[kRing];
+      auto pos = [&](int n, int& lm, int& gc) {
+        lm = wr0 + 16 * (n >> 2) + 4 * (n & 3) + (el >> 4);
+        gc = n0 + wn * 128 + (el & 15) * 8;
+      };
+      auto issue = [&](int n) {
+        int lm, gc;
+        pos(n, lm, gc);
+        const bool ok = lm < m_valid && gc < p.N;
+        // out-of-tile lanes read the tile's first valid element instead
+        const int64_t o = static_cast<int64_t>(row0 + (ok ? lm : 0)) * p.ldh +
+                          static_cast<int64_t>(ok ? gc : n0) * ES;
+        q1[n % kRing].load(p.H1 + o);
+        if constexpr (SW) q3[n % kRing].load(p.H3 + o);
+      };
+#pragma unroll
+      for (int n = 0; n < kPf; ++n) issue(n);
+#pragma unroll
+      for (int n = 0; n < kIt; ++n) {
+        if (n + kPf < kIt) issue(n + kPf);
+        if ((n & 3) == 0) stage16(strip, acc, n >> 2, el);
+        int lm, gc;
+        pos(n, lm, gc);
+        if (lm < m_valid && gc < p.N) {
+          const int r = 4 * (n & 3) + (el >> 4), c8 = (el & 15) * 8;
+          const int64_t grow = row0 + lm;
+          float h1[8], g1[8];
+          q1[n % kRing].to_f(h1);
+          if constexpr (SW) {
+            float h3[8], g3[8];
+            q3[n % kRing].to_f(h3);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float da = strip[r * kP16 + c8 + e];
+              const float sg = sigm(h1[e]);
+              g1[e] = da * h3[e] * sg * (1.f + h1[e] * (1.f - sg));
+              g3[e] = da * h1[e] * sg;
+            }
+            store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
+            store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(p.f + gc) * ES, g3);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              g1[e] = strip[r * kP16 + c8 + e] * act_grad_f(h1[e], p.act);
+            store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        stage16(strip, acc, i, el);
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+          const int r = 4 * it + (el >> 4), c8 = (el & 15) * 8;
+          const int lm = wr0 + 16 * i + r;
+          const int gc = n0 + wn * 128 + c8;
+          if (lm < m_valid && gc < p.N) {
+            const float* sp = strip + r * kP16 + c8;
+            if constexpr (MODE == M_DW) {
+              const int orow = row0 + lm;
+              float* dst;
+              if (slot >= 0) {
+                dst = p.partial + static_cast<int64_t>(slot) * p.slot_elems +
+                      static_cast<int64_t>(orow) * p.N + gc;
+              } else if (orow < p.split_row) {
+                dst = p.dwA + static_cast<int64_t>(g) * p.dw_gstride +
+                      static_cast<int64_t>(orow) * p.N + gc;
+              } else {
+                dst = p.dwB + static_cast<int64_t>(g) * p.dw_gstride +
+                      static_cast<int64_t>(orow - p.split_row) * p.N + gc;
+              }
+              *reinterpret_cast<float4*>(dst) = make_float4(sp[0], sp[1], sp[2], sp[3]);
+              *reinterpret_cast<float4*>(dst + 4) = make_float4(sp[4], sp[5], sp[6], sp[7]);
+            } else {
+              float v[8];
+#pragma unroll
+              for (int e = 0; e < 8; ++e) v[e] = sp[e];
+              const int64_t grow = row0 + lm;
+              if constexpr (MODE == M_FWD1) {
+                float hh[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                  hh[e] = Elem<T>::to_f(Elem<T>::from_f(v[e]));
+                  v[e] = act_f(hh[e], p.act);
+                }
+                if (p.H1) store_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, hh);
+              }
+              store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, v);
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();   // strips are free before the next tile's loads
+  }
+}
+
+// ---------------------------------------------------------------------------
 // split-K reduction
 // ---------------------------------------------------------------------------
 // dW[g] = sum over the expert's split slots, in slot order.  A bounded grid
@@ -939,7 +1412,7 @@ moe_status launch_gemm(hipStream_t s, moe_dtype dt, const GemmParams& p) {
   const int grid = persistent_grid();
   MOE_TIMED(pass_name(PASS), s);
   if (dt == MOE_BF16)
-    ffn_gemm_kernel<uint16_t, MODE, PASS><<<grid, kThreads, 0, s>>>(p);
+    ffn_gemm16_kernel<MODE, PASS><<<grid, kThreads16, 0, s>>>(p);
   else
     ffn_gemm_kernel<float, MODE, PASS><<<grid, kThreads, 0, s>>>(p);
   MOE_LAUNCH_CHECK();
