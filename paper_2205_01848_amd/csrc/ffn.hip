@@ -842,9 +842,9 @@ __device__ __forceinline__ void mfma16(floatx4& c, const uint4& a, const uint4& 
 // the loads into one stage from the reads of the other.
 template <int ALAY, int BLAY, bool GATED, bool FULL>
 __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* lb0, char* la1,
-                                           char* lb1, floatx4 (&acc)[8][8]) {
+                                           char* lb1, floatx4 (&acc)[8][8], int zt) {
   constexpr int KSTEP = 64;
-  const int lane = threadIdx.x & 63;
+  const int lane = (static_cast<int>(threadIdx.x) & 63) + zt;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
@@ -1124,11 +1124,16 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
       op.K = max(0, k1 - sg.y);
     }
 
+    // the main loop derives its per-lane constants from an opaque zero made
+    // per tile, so they are recomputed per tile instead of being hoisted out
+    // of the tile loop and spilled (their reloads would wait on the loads)
+    int zt;
+    asm volatile("s_mov_b32 %0, 0" : "=s"(zt));
     floatx4 acc[8][8];
     if (op.a.rows >= BM && op.b.rows >= (GATED ? BN / 2 : BN))
-      mainloop16<ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc);
+      mainloop16<ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc, zt);
     else
-      mainloop16<ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc);
+      mainloop16<ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc, zt);
 
     // Epilogue, wave by wave: 16 accumulator rows at a time go through the
     // wave's LDS strip; a lane then finishes 8 consecutive columns of a row
@@ -1141,6 +1146,10 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
     const int el = lane + z;
     float* strip = reinterpret_cast<float*>((wave < 2 ? la0 : lb0) + (wave & 1) * kStrip16Bytes + z);
     const int wr0 = wm * 128;                     // the wave's first tile row
+    // ReLU / GELU layers: the epilogue is specialised on the activation, one
+    // uniform branch per tile instead of one per element
+    auto epilogue = [&](auto act_c) {
+    constexpr int ACT = decltype(act_c)::value;
     if constexpr (MODE == M_FWD1_SWIGLU) {
       // strip columns [0,64): H1, [64,128): H3 of hidden units n0 + 64 wn + u
 #pragma unroll
@@ -1217,7 +1226,7 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
           } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-              g1[e] = strip[r * kP16 + c8 + e] * act_grad_f(h1[e], p.act);
+              g1[e] = strip[r * kP16 + c8 + e] * act_grad_f(h1[e], ACT);
             store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
           }
         }
@@ -1258,7 +1267,7 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                   hh[e] = Elem<T>::to_f(Elem<T>::from_f(v[e]));
-                  v[e] = act_f(hh[e], p.act);
+                  v[e] = act_f(hh[e], ACT);
                 }
                 if (p.H1) store_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, hh);
               }
@@ -1267,6 +1276,13 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
           }
         }
       }
+    }
+    };
+    if constexpr (MODE == M_FWD1 || MODE == M_BWD_DA) {
+      if (p.act == ACT_RELU) epilogue(std::integral_constant<int, ACT_RELU>{});
+      else epilogue(std::integral_constant<int, ACT_GELU>{});
+    } else {
+      epilogue(std::integral_constant<int, ACT_SWIGLU>{});
     }
     __syncthreads();   // strips are free before the next tile's loads
   }
