@@ -139,54 +139,118 @@ __device__ __forceinline__ float sigm(float h) { return rcp_fast(1.f + exp_fast(
 // ---------------------------------------------------------------------------
 // schedule
 // ---------------------------------------------------------------------------
-// One workgroup; thread 0 walks the experts in order.  Clamps every expert's
-// rows to its region and to rows_alloc, and the tile count to the host bound
-// the workspace was sized for, so no later kernel can index out of bounds.
-// The weight-gradient products split an expert's rows into K segments only
-// when few experts carry most rows (about 512 work items over all of them).
-__global__ void schedule_kernel(const int32_t* __restrict__ offsets,
-                                const int32_t* __restrict__ rows, int E,
-                                int64_t rows_alloc, int max_mtiles, int max_segs, int tmn_min,
-                                int max_slots, Sched* __restrict__ s, int2* __restrict__ mtile,
-                                int4* __restrict__ seg) {
-  if (threadIdx.x != 0) return;
-  int nm = 0;
-  int64_t kwork = 0;
-  for (int g = 0; g < E; ++g) {
+// Inclusive prefix sum over the 64 lanes of a wavefront.
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// One wavefront, lane g = expert g.  Clamps every expert's rows to its region
+// and to rows_alloc, and the tile count to the host bound the workspace was
+// sized for, so no later kernel can index out of bounds.  The weight-gradient
+// products split an expert's rows into K segments only when few experts
+// carry most rows (about 512 work items over all of them).  The experts'
+// tiles and segments are numbered in expert order by prefix sums; should a
+// bound be exceeded (inconsistent offsets), lane 0 instead walks the experts
+// in order and cuts the lists where the bounds stop them.
+__global__ __launch_bounds__(64) void schedule_kernel(
+    const int32_t* __restrict__ offsets, const int32_t* __restrict__ rows, int E,
+    int64_t rows_alloc, int max_mtiles, int max_segs, int tmn_min, int max_slots,
+    Sched* __restrict__ s, int2* __restrict__ mtile, int4* __restrict__ seg) {
+  const int g = threadIdx.x;
+  // rows of expert g, clamped to its region and to rows_alloc
+  int64_t m = 0;
+  if (g < E) {
     const int64_t off = offsets[g];
-    int64_t m = rows[g];
+    m = rows[g];
     if (off < 0 || off >= rows_alloc) m = 0;
     m = min(m, static_cast<int64_t>(offsets[g + 1]) - off);
     m = min(m, rows_alloc - off);
     m = max(m, int64_t(0));
-    m = min(m, static_cast<int64_t>(max_mtiles - nm) * BM);
-    const int mi = static_cast<int>(m);
-    s->rows[g] = mi;
-    for (int m0 = 0; m0 < mi; m0 += BM) mtile[nm++] = make_int2(g, m0);
-    kwork += (mi + kKc - 1) / kKc * kKc;
   }
-  s->n_mtiles = nm;
+  const int64_t tiles = (m + BM - 1) / BM;
+  const int64_t tiles_incl = wave_incl_scan(tiles);
+  const int64_t tiles_total = __shfl(tiles_incl, 63, 64);
+  const int64_t kw = (m + kKc - 1) / kKc * kKc;
+  const int64_t kwork = __shfl(wave_incl_scan(kw), 63, 64);
   int64_t kc = (kwork * tmn_min + 511) / 512;
   kc = (kc + kKc - 1) / kKc * kKc;
   kc = max(kc, static_cast<int64_t>(kSplitFloor));
-  int ns = 0, slots = 0;
-  for (int g = 0; g < E; ++g) {
-    const int kp = s->rows[g];
-    int nsp = kp > kc ? static_cast<int>((kp + kc - 1) / kc) : 1;
-    if (nsp > 1 && (slots + nsp > max_slots || ns + nsp > max_segs)) nsp = 1;
-    if (ns + nsp > max_segs) nsp = 0;  // cannot happen with host bounds; stay in bounds
-    s->nsplit[g] = nsp;
-    s->slot0[g] = nsp > 1 ? slots : -1;
-    for (int i = 0; i < nsp; ++i) {
-      const int k0 = static_cast<int>(min(static_cast<int64_t>(i) * kc, static_cast<int64_t>(kp)));
-      const int k1 = static_cast<int>(min(static_cast<int64_t>(i + 1) * kc, static_cast<int64_t>(kp)));
-      seg[ns++] = make_int4(g, nsp > 1 ? k0 : 0, nsp > 1 ? k1 : kp, nsp > 1 ? slots + i : -1);
+  const int64_t nsp = g < E ? (m > kc ? (m + kc - 1) / kc : 1) : 0;
+  const int64_t segs_incl = wave_incl_scan(nsp);
+  const int64_t slots_incl = wave_incl_scan(nsp > 1 ? nsp : 0);
+  // totals read from lane 63 while every lane is active
+  const int64_t segs_total = __shfl(segs_incl, 63, 64);
+  const int64_t slots_total = __shfl(slots_incl, 63, 64);
+  const bool fits = tiles_total <= max_mtiles && segs_total <= max_segs && slots_total <= max_slots;
+  if (fits) {
+    if (g < E) {
+      const int mi = static_cast<int>(m);
+      s->rows[g] = mi;
+      const int t0 = static_cast<int>(tiles_incl - tiles);
+      for (int i = 0; i < static_cast<int>(tiles); ++i) mtile[t0 + i] = make_int2(g, i * BM);
+      const int n = static_cast<int>(nsp);
+      const int s0 = static_cast<int>(segs_incl - nsp);
+      const int q0 = static_cast<int>(slots_incl - (n > 1 ? n : 0));
+      s->nsplit[g] = n;
+      s->slot0[g] = n > 1 ? q0 : -1;
+      for (int i = 0; i < n; ++i) {
+        const int k0 = static_cast<int>(min(static_cast<int64_t>(i) * kc, m));
+        const int k1 = static_cast<int>(min(static_cast<int64_t>(i + 1) * kc, m));
+        seg[s0 + i] = make_int4(g, n > 1 ? k0 : 0, n > 1 ? k1 : mi, n > 1 ? q0 + i : -1);
+      }
     }
-    if (nsp > 1) slots += nsp;
+    if (g == 0) {
+      s->n_mtiles = static_cast<int>(tiles_total);
+      s->n_segs = static_cast<int>(segs_total);
+      s->n_slots = static_cast<int>(slots_total);
+      s->kc = static_cast<int>(kc);
+    }
+    return;
+  }
+  if (g != 0) return;
+  int nm = 0;
+  int64_t kwork_c = 0;
+  for (int e = 0; e < E; ++e) {
+    const int64_t off = offsets[e];
+    int64_t me = rows[e];
+    if (off < 0 || off >= rows_alloc) me = 0;
+    me = min(me, static_cast<int64_t>(offsets[e + 1]) - off);
+    me = min(me, rows_alloc - off);
+    me = max(me, int64_t(0));
+    me = min(me, static_cast<int64_t>(max_mtiles - nm) * BM);
+    const int mi = static_cast<int>(me);
+    s->rows[e] = mi;
+    for (int m0 = 0; m0 < mi; m0 += BM) mtile[nm++] = make_int2(e, m0);
+    kwork_c += (mi + kKc - 1) / kKc * kKc;
+  }
+  s->n_mtiles = nm;
+  int64_t kcc = (kwork_c * tmn_min + 511) / 512;
+  kcc = (kcc + kKc - 1) / kKc * kKc;
+  kcc = max(kcc, static_cast<int64_t>(kSplitFloor));
+  int ns = 0, slots = 0;
+  for (int e = 0; e < E; ++e) {
+    const int kp = s->rows[e];
+    int ne = kp > kcc ? static_cast<int>((kp + kcc - 1) / kcc) : 1;
+    if (ne > 1 && (slots + ne > max_slots || ns + ne > max_segs)) ne = 1;
+    if (ns + ne > max_segs) ne = 0;
+    s->nsplit[e] = ne;
+    s->slot0[e] = ne > 1 ? slots : -1;
+    for (int i = 0; i < ne; ++i) {
+      const int k0 = static_cast<int>(min(static_cast<int64_t>(i) * kcc, static_cast<int64_t>(kp)));
+      const int k1 = static_cast<int>(min(static_cast<int64_t>(i + 1) * kcc, static_cast<int64_t>(kp)));
+      seg[ns++] = make_int4(e, ne > 1 ? k0 : 0, ne > 1 ? k1 : kp, ne > 1 ? slots + i : -1);
+    }
+    if (ne > 1) slots += ne;
   }
   s->n_segs = ns;
   s->n_slots = slots;
-  s->kc = static_cast<int>(kc);
+  s->kc = static_cast<int>(kcc);
 }
 
 // ---------------------------------------------------------------------------
@@ -1295,8 +1359,10 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
 // strides over the elements (blockIdx.y = expert), so experts without a
 // split cost one early exit per block rather than a launch per 1024
 // elements.
-constexpr int kReduceBlocks = 256;   // blocks per expert
+constexpr int kReduceBlocks = 1024;   // blocks per expert
 
+// The slots are added in slot order; their loads are issued four at a time
+// ahead of the adds, so a thread waits out one memory latency per four slots.
 __global__ __launch_bounds__(256) void split_reduce_kernel(
     const float* __restrict__ partial, int64_t slot_elems, const Sched* __restrict__ sc,
     float* __restrict__ dwA, float* __restrict__ dwB, int64_t dw_gstride, int split_row,
@@ -1305,15 +1371,30 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(
   const int ns = sc->nsplit[g];
   if (ns <= 1) return;
   const float* base = partial + static_cast<int64_t>(sc->slot0[g]) * slot_elems;
+  auto add = [](float4& a, const float4& v) { a.x += v.x; a.y += v.y; a.z += v.z; a.w += v.w; };
   for (int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4; i < slot_elems;
        i += static_cast<int64_t>(gridDim.x) * 1024) {
     const float* p0 = base + i;
     float4 acc = *reinterpret_cast<const float4*>(p0);
-    for (int s = 1; s < ns; ++s) {
-      const float4 v = *reinterpret_cast<const float4*>(p0 + static_cast<int64_t>(s) * slot_elems);
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    int sl = 1;
+    for (; sl + 3 < ns; sl += 4) {
+      float4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        v[u] = *reinterpret_cast<const float4*>(p0 + static_cast<int64_t>(sl + u) * slot_elems);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add(acc, v[u]);
     }
-    const int64_t row = i / N, col = i % N;
+    for (; sl < ns; ++sl) add(acc, *reinterpret_cast<const float4*>(p0 + static_cast<int64_t>(sl) * slot_elems));
+    int64_t row, col;
+    if (slot_elems < (int64_t(1) << 31)) {   // the usual case: 32-bit division
+      const uint32_t ii = static_cast<uint32_t>(i);
+      row = ii / static_cast<uint32_t>(N);
+      col = ii % static_cast<uint32_t>(N);
+    } else {
+      row = i / N;
+      col = i % N;
+    }
     float* dst = row < split_row
                      ? dwA + static_cast<int64_t>(g) * dw_gstride + row * N + col
                      : dwB + static_cast<int64_t>(g) * dw_gstride + (row - split_row) * N + col;

@@ -300,13 +300,19 @@ __global__ __launch_bounds__(64) void gate_bwd_dlogits_kernel(
 }
 
 // dw_g partial sums: block = 64 threads x 8 columns = 512 columns, 8 experts,
-// one chunk of kGbTok tokens.  grid = (E/8 groups, d/512, chunks).
-constexpr int kGbTok = 256;
+// one chunk of kGbTok tokens.  grid = (E/8 groups, d/512, chunks).  The
+// tokens of a chunk are taken kGbBatch at a time: the batch's x vectors are
+// loaded before any of them is used, so the loads overlap instead of each
+// waiting out its own latency.  Per column the sum runs over the tokens in
+// order (batching changes only when the loads are issued).
+constexpr int kGbTok = 128;
+constexpr int kGbBatch = 8;
 
 template <typename T>
 __global__ __launch_bounds__(64) void gate_bwd_dwg_partial_kernel(
     const T* __restrict__ x, const float* __restrict__ dl, int Ttok, int d,
     int E, float* __restrict__ part) {
+  constexpr int kVecs = sizeof(T) / 2;   // 16-byte vectors per 8 elements
   const int eg = blockIdx.x * 8;
   const int c0 = (blockIdx.y * 64 + threadIdx.x) * 8;
   const int chunk = blockIdx.z;
@@ -317,28 +323,36 @@ __global__ __launch_bounds__(64) void gate_bwd_dwg_partial_kernel(
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[e][c] = 0.f;
   const bool colok = c0 < d;
-  for (int t = tb; t < te; ++t) {
-    float xv[8];
-    if (colok) {
-      const T* xr = x + static_cast<size_t>(t) * d + c0;
-      if constexpr (sizeof(T) == 2) {
-        unpack8(*reinterpret_cast<const uint4*>(xr), xv);
-      } else {
-        const uint4 a = *reinterpret_cast<const uint4*>(xr);
-        const uint4 b = *reinterpret_cast<const uint4*>(xr + 4);
-        Elem<float>::load(a, xv);
-        Elem<float>::load(b, xv + 4);
+  for (int t0 = tb; t0 < te; t0 += kGbBatch) {
+    uint4 raw[kGbBatch][kVecs];
+#pragma unroll
+    for (int u = 0; u < kGbBatch; ++u) {
+      const int t = t0 + u;
+#pragma unroll
+      for (int v = 0; v < kVecs; ++v) {
+        raw[u][v] = (colok && t < te)
+                        ? reinterpret_cast<const uint4*>(x + static_cast<size_t>(t) * d + c0)[v]
+                        : make_uint4(0u, 0u, 0u, 0u);
       }
-    } else {
-#pragma unroll
-      for (int c = 0; c < 8; ++c) xv[c] = 0.f;
     }
-    const float* dlr = dl + static_cast<size_t>(t) * E + eg;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float g = (eg + e < E) ? dlr[e] : 0.f;
+    for (int u = 0; u < kGbBatch; ++u) {
+      const int t = t0 + u;
+      if (t >= te) break;
+      float xv[8];
+      if constexpr (sizeof(T) == 2) {
+        unpack8(raw[u][0], xv);
+      } else {
+        Elem<float>::load(raw[u][0], xv);
+        Elem<float>::load(raw[u][kVecs - 1], xv + 4);
+      }
+      const float* dlr = dl + static_cast<size_t>(t) * E + eg;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) acc[e][c] = fmaf(g, xv[c], acc[e][c]);
+      for (int e = 0; e < 8; ++e) {
+        const float g = (eg + e < E) ? dlr[e] : 0.f;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[e][c] = fmaf(g, xv[c], acc[e][c]);
+      }
     }
   }
   if (!colok) return;
@@ -351,13 +365,21 @@ __global__ __launch_bounds__(64) void gate_bwd_dwg_partial_kernel(
   }
 }
 
-// dw_g[e,i] = sum over chunks in order
+// dw_g[e,i] = sum over chunks in order (loads issued 8 chunks ahead of the adds)
 __global__ __launch_bounds__(256) void gate_bwd_dwg_reduce_kernel(
     const float* __restrict__ part, int nchunks, int n, float* __restrict__ dwg) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   float s = 0.f;
-  for (int c = 0; c < nchunks; ++c) s += part[static_cast<size_t>(c) * n + i];
+  int c = 0;
+  for (; c + 8 <= nchunks; c += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = part[static_cast<size_t>(c + u) * n + i];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  for (; c < nchunks; ++c) s += part[static_cast<size_t>(c) * n + i];
   dwg[i] = s;
 }
 

@@ -21,7 +21,7 @@
 namespace moe {
 namespace {
 
-constexpr int kChunk = 4096;  // assignments per workgroup in the routing kernels
+constexpr int kChunk = 1024;  // assignments per workgroup in the routing kernels
 
 // Is assignment (t, j) live?  Sets status bits when `status` is non-null.
 __device__ __forceinline__ bool live_assignment(const int32_t* __restrict__ ids, int t,
@@ -129,7 +129,18 @@ __global__ __launch_bounds__(64) void route_scan_kernel(
   const int e = threadIdx.x;
   if (e >= E) return;
   int run = 0;
-  for (int b = 0; b < nblk; ++b) {
+  int b = 0;
+  for (; b + 8 <= nblk; b += 8) {   // loads of 8 chunks issued before their adds
+    int h[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) h[u] = hist[static_cast<size_t>(b + u) * E + e];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      base[static_cast<size_t>(b + u) * E + e] = run;
+      run += h[u];
+    }
+  }
+  for (; b < nblk; ++b) {
     base[static_cast<size_t>(b) * E + e] = run;
     run += hist[static_cast<size_t>(b) * E + e];
   }
