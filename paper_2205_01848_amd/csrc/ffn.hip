@@ -6,8 +6,8 @@
 // 256x256 output tiles, K tiles of 128 bytes, operand tiles loaded HBM ->
 // LDS by buffer loads, double-buffered, with an XOR swizzle that keeps the
 // MFMA fragment reads bank-conflict free.
-//  * bf16 layers: 4 wavefronts of 128x128 on v_mfma_f32_16x16x32_bf16, one
-//    barrier per K step, loads and fragment reads issued one at a time
+//  * bf16 layers: 4 wavefronts of 128x128 on v_mfma_f32_16x16x32_bf16, two
+//    barriers per K step, loads and fragment reads issued one at a time
 //    between the MFMAs (ffn_gemm16_kernel).
 //  * fp32 layers: 8 wavefronts of 128x64 on v_mfma_f32_32x32x2f32 in two
 //    ping-pong teams, one team's MFMAs overlapping the other's LDS reads
@@ -873,11 +873,13 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
 // bf16 layers run every product on 4 wavefronts, one per SIMD, each holding a
 // 128x128 block of the 256x256 tile as 64 blocks of 16x16 fp32 accumulators
 // (v_mfma_f32_16x16x32_bf16, 256 accumulation registers).  Per K step of 64
-// there is one barrier.  Between the MFMAs each wave issues, one at a time,
-// the fragment reads of the next half step and, after the barrier, its share
-// of the direct-to-LDS loads of the step after next, so the memory pipeline
-// sees a steady stream of requests while the matrix core stays busy.  A
-// 128x128 block reads a third less LDS per MFMA than a 128x64 one.
+// there are two barriers, one after the A and one after the B fragment reads
+// of the step's stage.  Between the MFMAs each wave issues, one at a time,
+// the fragment reads of the next half step and, once a barrier has freed its
+// part of the stage, its share of the direct-to-LDS loads of the step after
+// next, so the memory pipeline sees a steady stream of requests while the
+// matrix core stays busy.  A 128x128 block reads a third less LDS per MFMA
+// than a 128x64 one.
 constexpr int kThreads16 = 256;
 constexpr int kP16 = 132;                      // floats per staged row (128 + 4)
 constexpr int kStrip16Bytes = 16 * kP16 * 4;   // 16 rows: two strips per 32 KB array
@@ -1046,13 +1048,17 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
   bool active = true;
   if constexpr (!FULL) active = wm * 128 < op.a.rows && wn * (GATED ? 64 : 128) < op.b.rows;
 
-  constexpr int kPre = 8;   // MFMAs of the second half before the barrier
-  // One K step from stage (ca, cb), the next stage in (na, nb); loads of step
-  // kt + 2 go into (ca, cb) once every wave has finished reading it.
+  // One K step from stage (ca, cb), the next stage in (na, nb); the loads of
+  // step kt + 2 go into (ca, cb): its A part once every wave has read the A
+  // fragments of k-half 1, its B part once every wave has read the B ones.
+  // Two barriers per step let the 16 loads spread over the last three
+  // quarters of the step (one per 6 MFMAs) instead of crowding into the
+  // second half.
   auto step = [&](int kt, char* ca, char* cb, const char* na, const char* nb) {
-    // first half: MFMAs of k-half 0, one read of k-half 1 per 4 MFMAs
+    const StepLd s = step_ld(kt + 2);
+    // first quarter: MFMAs 0..31 of k-half 0, reads of the A fragments of k-half 1
 #pragma unroll
-    for (int g = 0; g < 16; ++g) {
+    for (int g = 0; g < 8; ++g) {
       if (active) {
         read1(ca, cb, 1, f1a, f1b, g);
 #pragma unroll
@@ -1060,27 +1066,36 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    // second half: kPre MFMAs, then wait for stage kt+1 and for every wave's
-    // reads of stage kt; then this wave's loads of step kt+2, the reads of
-    // the next stage's k-half 0 and the remaining MFMAs, interleaved
-    const StepLd s = step_ld(kt + 2);
-    if (active) {
-#pragma unroll
-      for (int m = 0; m < kPre; ++m) mfma16(acc[m >> 3][m & 7], f1a[m >> 3], f1b[m & 7]);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    constexpr int kRest = 64 - kPre;
+    // second quarter: MFMAs 32..63 of k-half 0, reads of the B fragments of
+    // k-half 1, the A loads of step kt + 2
+#pragma unroll
+    for (int g = 8; g < 16; ++g) {
+      // A loads 0..5 at groups 8, 9, 11, 12, 14, 15
+      if (g % 3 != 1) load1(s, ca, cb, g - 8 - (g - 8) / 3);
+      if (active) {
+        read1(ca, cb, 1, f1a, f1b, g);
+#pragma unroll
+        for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f0a[m >> 3], f0b[m & 7]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // stage kt + 1 has landed (only the 6 A loads just issued may be pending)
+    __builtin_amdgcn_s_waitcnt(0x0076);   // vmcnt(6) lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    // second half: MFMAs of k-half 1, reads of the next stage's k-half 0, the
+    // B loads of step kt + 2
 #pragma unroll
     for (int g = 0; g < 16; ++g) {
-      load1(s, ca, cb, g);
+      // A loads 6, 7 and the B loads at groups 0, 2, 3, 5, 6, 8, 9, 11, 12, 14
+      if (g % 3 != 1 && g < 15) load1(s, ca, cb, 6 + g - (g + 1) / 3);
       if (active) {
         read1(na, nb, 0, f0a, f0b, g);
 #pragma unroll
-        for (int m = kPre + kRest * g / 16; m < kPre + kRest * (g + 1) / 16; ++m)
-          mfma16(acc[m >> 3][m & 7], f1a[m >> 3], f1b[m & 7]);
+        for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f1a[m >> 3], f1b[m & 7]);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
