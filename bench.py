@@ -41,7 +41,7 @@ VARIANTS = {
     "policy": "capacities from the host launch-frontier policy (pinned counts ring)",
 }
 # bounded oracle sample (tokens) per workload, about 10-30 s of CPU work
-CPU_SAMPLE = {"c1": 256, "c2": 8192, "c3": 16384, "c4": 2048, "c5": 512}
+CPU_SAMPLE = {"c1": 256, "c2": 8192, "c3": 16384, "c4": 2048, "c5": 4096}
 
 
 def log(msg):
