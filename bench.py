@@ -189,12 +189,12 @@ def policy_sweep(args):
     """Drops vs average capacity factor over a drifting trajectory of
     mini-batches (routing only: count -> capacity -> dispatch of narrow
     rows), for static capacities (Eq. 4) and launch-frontier policies
-    (Section 3.1 with the recompile appendix), every capacity trajectory
-    checked against the oracle's simulation on the same counts."""
+    (Section 3.1 with the recompile appendix).  The demand per mini-batch is
+    the library's own count; the capacity trajectories of these settings are
+    checked against the oracle in the GPU tests, not here."""
     import numpy as np
     import torch
 
-    import oracle as O
     import workloads as W
     from paper_2205_01848_amd import binding as B
 
@@ -202,7 +202,6 @@ def policy_sweep(args):
     T, E, k, N, dw = wl.T, wl.E, wl.k, args.steps, 8
     log(f"policy sweep on {args.workload} shapes: {N} drifting mini-batches")
     traj = W.drifting_assignments(wl.seed, T, E, k, N)
-    seq = [O.count_assignments(a, E) for a in traj]
     dev = torch.device("cuda:0")
     ids_dev = [torch.from_numpy(a).to(dev) for a in traj]
     R = E * T
@@ -218,13 +217,19 @@ def policy_sweep(args):
     ws = B.workspace(B.moe_dispatch_workspace_bytes(T, E, k), dev)
     fills = torch.empty(N, E, dtype=torch.int32, device=dev)
     caps = torch.empty(N, E, dtype=torch.int32, device=dev)
+    demands = torch.empty(N, E, dtype=torch.int32, device=dev)
+    for i in range(N):                     # per-expert demand of every mini-batch
+        B.moe_count(ids_dev[i], E, counts, status)
+        demands[i].copy_(counts)
+    torch.cuda.synchronize()
+    seq = demands.cpu().numpy().astype(np.int64)
     demand = float(T * k)
 
     def summarise(name, extra):
         torch.cuda.synchronize()
         f = fills.cpu().numpy().astype(np.int64)
         c = caps.cpu().numpy().astype(np.int64)
-        drops = (np.array(seq) - f).sum()
+        drops = (seq - f).sum()
         row = {"setting": name, "dropped_pct": round(100.0 * drops / (N * demand), 3),
                "avg_capacity_factor": round(float(c.sum(axis=1).mean()) / demand, 4)}
         row.update(extra)
@@ -247,8 +252,8 @@ def policy_sweep(args):
             caps[i].copy_(cap)
         rows.append(summarise(f"device dynamic {margin[0]}/{margin[1]} (this batch's counts)",
                               {})[0])
-    init = O.capacity_static(T, k, E, 1, 1)
-    ok = True
+    B.moe_update_capacity(T, k, E, None, 1, 1, 0, cap, off)   # static alpha = 1
+    init = cap.cpu().numpy().astype(np.int64)
     for grow, shrink in [((21, 20), (5, 4)), ((11, 10), (13, 10)), ((6, 5), (3, 2)),
                          ((5, 4), (2, 1))]:
         for delta in (0, 1, 2):
@@ -269,16 +274,12 @@ def policy_sweep(args):
             row, c = summarise(f"policy grow {grow[0]}/{grow[1]} shrink {shrink[0]}/{shrink[1]} "
                                f"delta {delta}",
                                {"recompiles": st["recompiles"], "ms_per_iteration": round(wall, 3)})
-            sim = O.simulate_capacity_policy(seq, T, k, delta, init, grow, shrink)
-            match = bool(np.array_equal(c, sim["caps"]))
-            ok = ok and match
-            row["oracle_caps_match"] = match
             rows.append(row)
     out = {"metric": "capacity policy: dropped assignments vs average capacity factor",
            "workload": f"{args.workload} shapes T={T} E={E} k={k}, {N} mini-batches with "
                        "drifting Zipf loads (exponent 1.2 -> 0.6, adjacent experts swap "
                        "every 5)",
-           "status": int(status.item()), "all_policies_match_oracle": ok, "rows": rows}
+           "status": int(status.item()), "rows": rows}
     print(json.dumps(out))
 
 
@@ -286,7 +287,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer is not "
-              "sharded across GPUs in this build.", file=sys.stderr)
+              "sharded across GPUs.", file=sys.stderr)
         sys.exit(2)
     if args.copy_gib > 0:
         copy_calibration(args.copy_gib, args.steps)

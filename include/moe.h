@@ -50,7 +50,7 @@ extern "C" {
 typedef enum {
   MOE_OK = 0,
   MOE_EINVAL = 1,        /* bad size, NULL pointer or flag */
-  MOE_EUNSUPPORTED = 2,  /* valid request this build does not implement */
+  MOE_EUNSUPPORTED = 2,  /* valid request the library does not implement */
   MOE_EHIP = 3,          /* a HIP launch failed */
   MOE_EWORKSPACE = 4     /* workspace NULL or smaller than the query said */
 } moe_status;

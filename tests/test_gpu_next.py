@@ -296,12 +296,19 @@ def test_forward_cached_with_concurrent_gate(concurrent):
 
 
 # ---- capacity policy at the launch frontier ---------------------------------------
+# the grow / shrink settings of the benchmark's policy sweep, on its two shapes
+# (T, E, k of the largest layer and of the 64-expert top-1 layer)
+POLICY_SETTINGS = [((21, 20), (5, 4)), ((11, 10), (13, 10)), ((6, 5), (3, 2)), ((5, 4), (2, 1))]
+
+
 @pytest.mark.parametrize("delta", [0, 1, 3])
-def test_capacity_policy_on_device_counts(delta):
-    T, E, k, d, N = 4096, 8, 2, 64, 24
+@pytest.mark.parametrize("setting", range(len(POLICY_SETTINGS)))
+@pytest.mark.parametrize("shape", [(4096, 8, 2), (16384, 64, 1)])
+def test_capacity_policy_on_device_counts(delta, setting, shape):
+    (T, E, k), d, N = shape, 64, 24
     traj = W.drifting_assignments(9, T, E, k, N)
     init = O.capacity_static(T, k, E, 1, 1)
-    grow, shrink = (11, 10), (13, 10)
+    grow, shrink = POLICY_SETTINGS[setting]
     pol = B.CapacityPolicy(T, k, E, delta, grow, shrink, init)
     R = E * T                                   # any capacity the policy can choose fits
     x = torch.zeros(T, d, dtype=torch.bfloat16, device=dev())
@@ -339,7 +346,7 @@ def test_capacity_policy_on_device_counts(delta):
     np.testing.assert_array_equal(drops, sim["drops"])
     # begin() of iteration i consumes the metrics up to iteration i - 1 - delta
     assert st["launched"] == N and st["consumed"] == N - 1 - delta
-    assert st["recompiles"] == int(sim["recompile"].sum()) > 0
+    assert st["recompiles"] == int(sim["recompile"].sum())
     assert int(status.item()) == 0
 
 
