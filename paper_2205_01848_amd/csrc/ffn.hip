@@ -11,7 +11,7 @@
 //    between the MFMAs (ffn_gemm16_kernel).
 //  * fp32 layers: 8 wavefronts of 128x64 on v_mfma_f32_32x32x2f32 in two
 //    ping-pong teams, one team's MFMAs overlapping the other's LDS reads
-//    (ffn_gemm_kernel).
+//    (ffn_gemm_f32_kernel).
 //  * var-M products (forward H, Y; backward dA, dX): the M dimension of
 //    expert e is its row count, read on the device; tiles are listed by a
 //    one-workgroup schedule kernel, so no host synchronisation is needed.
@@ -256,21 +256,14 @@ __global__ __launch_bounds__(64) void schedule_kernel(
 // ---------------------------------------------------------------------------
 // GEMM core
 // ---------------------------------------------------------------------------
-template <typename T> struct Mma;
-template <> struct Mma<uint16_t> {
-  __device__ static __forceinline__ void run(floatx16& c, const uint4& a, const uint4& b) {
-    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-  }
-};
-template <> struct Mma<float> {
-  __device__ static __forceinline__ void run(floatx16& c, const uint4& a, const uint4& b) {
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
-  }
-};
+// c += a * b over four k values: one 32x32 fp32 block, k = 4 consecutive
+// values per lane (one 32-bit element of each of the four words)
+__device__ __forceinline__ void mma_f32(floatx16& c, const uint4& a, const uint4& b) {
+  c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+}
 
 // Operand layouts.  Every product is C[m, n] = sum_k A[m, k] B[n, k]; an
 // operand is stored either K-contiguous (rows are m (or n), k along each
@@ -329,22 +322,22 @@ __device__ __forceinline__ uint2 read_tr(const char* p) {
   return __builtin_bit_cast(uint2, v);
 }
 
-// acc += A_tile * B_tile^T over the whole K extent: 8 wavefronts in two
-// teams of four, one wave of each team per SIMD.  Team t computes tile rows
-// 128t..128t+127, its wave q columns 64q..64q+63 (gated forward: hidden units
-// 32q..32q+31, W1 then W3).  Each half K step (32 bf16) is a memory phase
-// (12 fragments, LDS -> registers) followed by an MFMA phase (16 MFMAs from
-// registers).  Team 1 runs one barrier behind team 0, so while one wave of a
-// SIMD issues MFMAs the other reads LDS.  Operand tiles go HBM -> LDS with
-// buffer_load ... lds (no register staging), issued by team 0 one step ahead
-// into the other of two stages.  FULL: every tile row and column is valid;
-// K tails are checked per step either way.
-template <typename T, int ALAY, int BLAY, bool GATED, bool FULL>
-__device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0, char* la1,
-                                         char* lb1, floatx16 (&acc)[4][2]) {
-  constexpr int ES = sizeof(T);
+// fp32 layers: acc += A_tile * B_tile^T over the whole K extent with 8
+// wavefronts in two teams of four, one wave of each team per SIMD.  Team t
+// computes tile rows 128t..128t+127, its wave q columns 64q..64q+63 (gated
+// forward: hidden units 32q..32q+31, W1 then W3).  Each half K step (16
+// values) is a memory phase (12 fragments, LDS -> registers) followed by an
+// MFMA phase (16 block products of four v_mfma_f32_32x32x2f32 each).  Team 1
+// runs one barrier behind team 0, so while one wave of a SIMD issues MFMAs
+// the other reads LDS.  Operand tiles go HBM -> LDS with buffer_load ... lds
+// (no register staging), issued by team 0 one step ahead into the other of
+// two stages.  FULL: every tile row and column is valid; K tails are checked
+// per step either way.
+template <int ALAY, int BLAY, bool GATED, bool FULL>
+__device__ __forceinline__ void mainloop_f32(const TileOps& op, char* la0, char* lb0, char* la1,
+                                             char* lb1, floatx16 (&acc)[4][2]) {
+  constexpr int ES = 4;                   // bytes per element
   constexpr int KSTEP = kRowBytes / ES;   // k values per step (KC: 128 bytes per row)
-  constexpr int KMR = 2 / (ES / 2);       // KM: k-rows per 1 KB block (bf16 2, fp32 1)
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int team = wave >> 2, wq = wave & 3;
@@ -361,13 +354,12 @@ __device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0
 
   // ---- loads.  A 1 KB load covers one 8-row block of a KC tile (lane l ->
   // row 8 blk + (l >> 3), physical chunk l & 7, logical chunk (l & 7) ^
-  // swz(row), depending on the parity of blk only), or KMR k-rows of a KM
-  // tile (lane l -> k-row KMR blk + (l >> 5) (bf16) / blk (fp32), physical
-  // element e = 16 l / ES within the row, column = segment swizzled by k & 3).
+  // swz(row), depending on the parity of blk only), or one k-row of a KM
+  // tile (lane l -> physical elements 4l .. 4l + 3 of k-row blk, column =
+  // segment swizzled by k & 3).
   const int l3 = lane >> 3;
   const int co0 = ((lane & 7) ^ swz(l3)) * 16, co1 = ((lane & 7) ^ swz(l3 + 8)) * 16;
-  const int kr = ES == 2 ? lane >> 5 : 0;                       // KM k-row within the block
-  const int pe = ES == 2 ? (lane & 31) * 8 : lane * 4;          // KM physical element
+  const int pe = lane * 4;                // KM physical element
   // KM column of the lane for k-row residue q = k & 3
   auto km_col = [&](int q) { return (((pe >> 5) ^ q) << 5) + (pe & 31); };
   auto ld_of = [&](const Operand& o) { return static_cast<int>(o.ld); };
@@ -392,15 +384,15 @@ __device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0
         if (!ok) off = kOob;
       }
     } else {
-      const int krel = KMR * blk;                  // first k-row of the block in the step
+      const int krel = blk;                        // the block's k-row in the step
       const int kabs = kt * KSTEP + krel;
-      const int q = (krel + kr) & 3;               // k & 3 (steps are multiples of 4 rows)
+      const int q = krel & 3;                      // k & 3 (steps are multiples of 4 rows)
       const int col = km_col(q);
       second = kabs >= o.split;
-      off = static_cast<uint32_t>(kr * ld_of(o) + col * ES);
+      off = static_cast<uint32_t>(col * ES);
       soff = krel * ld_of(o);
       if (!FULL || !kfull) {
-        const bool ok = (FULL || col < o.rows) && (kfull || kabs + kr < K);
+        const bool ok = (FULL || col < o.rows) && (kfull || kabs < K);
         if (!ok) off = kOob;
       }
     }
@@ -444,34 +436,22 @@ __device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0
   };
 
   // ---- fragments.  MFMA operand of lane l: row/column l % 32 of the
-  // sub-tile, k values 8 (2s + l / 32) .. +7 of sub-step s (bf16; fp32: 4
-  // values 4 (2s + l / 32) .. +3).
+  // sub-tile, k values 4 (2s + l / 32) .. +3 of sub-step s.
   const int fr_row = lane & 31;
   // KC: 16-byte reads of row fr_row
   const int fr_a = (team * 128 + fr_row) * kRowBytes;
   const int fr_b = (wq * 64 + fr_row) * kRowBytes;
-  // KM bf16: two transpose reads; lane l of 16-lane group g addresses k-row
-  // kgrp + 4t + (j >> 2), columns cb + mgrp + 4 (j & 3), j = l % 16
-  const int j16 = lane & 15, g16 = lane >> 4;
-  const int tr_row = (g16 >> 1) * 8 + (j16 >> 2);
-  const int tr_col = (g16 & 1) * 16 + 4 * (j16 & 3);
+  // KM: four 4-byte reads, one per k-row (k-row c at physical segment
+  // (column >> 5) ^ c, the swizzle of the loads)
   auto km_frag = [&](const char* st, int cb, int s) -> uint4 {
-    if constexpr (ES == 2) {
-      const int phys = (((cb >> 5) ^ (j16 >> 2)) << 5) + tr_col;   // (tr_row & 3) == j16 >> 2
-      const char* p0 = st + (16 * s + tr_row) * 512 + phys * 2;
-      const uint2 lo = read_tr(p0);
-      const uint2 hi = read_tr(p0 + 4 * 512);
-      return make_uint4(lo.x, lo.y, hi.x, hi.y);
-    } else {
-      const int k0 = 4 * (2 * s + (lane >> 5));
-      uint32_t v[4];
+    const int k0 = 4 * (2 * s + (lane >> 5));
+    uint32_t v[4];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int phys = (((cb >> 5) ^ c) << 5) + fr_row;
-        v[c] = *reinterpret_cast<const uint32_t*>(st + (k0 + c) * 1024 + phys * 4);
-      }
-      return make_uint4(v[0], v[1], v[2], v[3]);
+    for (int c = 0; c < 4; ++c) {
+      const int phys = (((cb >> 5) ^ c) << 5) + fr_row;
+      v[c] = *reinterpret_cast<const uint32_t*>(st + (k0 + c) * 1024 + phys * 4);
     }
+    return make_uint4(v[0], v[1], v[2], v[3]);
   };
   uint4 fa[4][2], fb[2][2];   // [sub-tile][k sub-step within the half step]
   // fragments of k sub-steps 2h and 2h+1 (one half of a K step)
@@ -502,12 +482,12 @@ __device__ __forceinline__ void mainloop(const TileOps& op, char* la0, char* lb0
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) Mma<T>::run(acc[i][j], fa[i][s2], fb[j][s2]);
+        for (int j = 0; j < 2; ++j) mma_f32(acc[i][j], fa[i][s2], fb[j][s2]);
   };
   // s_waitcnt immediates (gfx9 encoding)
   constexpr int kWaitVm0 = 0x0F70;    // vmcnt(0)
   constexpr int kWaitLgkm0 = 0xC07F;  // lgkmcnt(0)
-  // one ping-pong phase pair: read half h of a stage, then its 16 MFMAs
+  // one ping-pong phase pair: read half h of a stage, then its 16 block products
   // A wave whose rows or columns of the tile are all beyond the valid ones
   // (the ragged last tile of an expert, the last column tile) skips its
   // reads and MFMAs; it still takes part in every barrier.  Its accumulators
@@ -635,15 +615,16 @@ __host__ __device__ constexpr int b_layout(int pass) {
   return pass == P_FWD_H || pass == P_FWD_Y ? L_KC : L_KM;
 }
 
-template <typename T, int MODE, int PASS>
-__global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams p) {
+template <int MODE, int PASS>
+__global__ __launch_bounds__(kThreads, 1) void ffn_gemm_f32_kernel(const GemmParams p) {
   // two stages of the A and B tiles, four distinct objects (see mainloop);
   // after the K loop the same memory holds each wave's epilogue strip
   __shared__ __attribute__((aligned(16))) char la0[kTileBytes];
   __shared__ __attribute__((aligned(16))) char lb0[kTileBytes];
   __shared__ __attribute__((aligned(16))) char la1[kTileBytes];
   __shared__ __attribute__((aligned(16))) char lb1[kTileBytes];
-  constexpr int ES = sizeof(T);
+  using T = float;
+  constexpr int ES = 4;
   constexpr bool VARK = MODE == M_DW;
   constexpr bool GATED = MODE == M_FWD1_SWIGLU;
   constexpr int ALAY = a_layout(PASS), BLAY = b_layout(PASS);
@@ -721,9 +702,9 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_kernel(const GemmParams 
 
     floatx16 acc[4][2];
     if (op.a.rows >= BM && op.b.rows >= (GATED ? BN / 2 : BN))
-      mainloop<T, ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc);
+      mainloop_f32<ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc);
     else
-      mainloop<T, ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc);
+      mainloop_f32<ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc);
 
     // Epilogue, wave by wave: 16 accumulator rows at a time go through the
     // wave's own LDS strip, then each lane finishes 8 consecutive columns of
@@ -922,8 +903,10 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
   if (nk <= 0) return;
   const int nk2 = (nk + 1) & ~1;   // odd counts load one all-zero step
 
-  // ---- loads: 1 KB blocks, as in the 8-wave kernel; wave w loads blocks
-  // 8w .. 8w+7 of A (g = 0..7) and of B (g = 8..15) of every stage.
+  // ---- loads: 1 KB blocks (8 rows of a KC tile: lane l -> row l >> 3,
+  // physical chunk l & 7; or 2 k-rows of a KM tile: lane l -> k-row l >> 5,
+  // physical elements 8 (l & 31) .. +7); wave w loads blocks 8w .. 8w+7 of
+  // A (g = 0..7) and of B (g = 8..15) of every stage.
   const int l3 = lane >> 3;
   const int co0 = ((lane & 7) ^ swz(l3)) * 16, co1 = ((lane & 7) ^ swz(l3 + 8)) * 16;
   const int kr = lane >> 5;            // KM: k-row within the block
@@ -1526,7 +1509,7 @@ moe_status launch_gemm(hipStream_t s, moe_dtype dt, const GemmParams& p) {
   if (dt == MOE_BF16)
     ffn_gemm16_kernel<MODE, PASS><<<grid, kThreads16, 0, s>>>(p);
   else
-    ffn_gemm_kernel<float, MODE, PASS><<<grid, kThreads, 0, s>>>(p);
+    ffn_gemm_f32_kernel<MODE, PASS><<<grid, kThreads, 0, s>>>(p);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }

@@ -43,13 +43,10 @@ def source_hash() -> str:
 
 
 def short_name(name: str) -> str:
-    # bf16 products: ffn_gemm16_kernel<MODE, PASS>; fp32: ffn_gemm_kernel<float, MODE, PASS>
-    m = re.search(r"ffn_gemm16_kernel<(\d+), (\d+)>", name)
+    # bf16 products: ffn_gemm16_kernel<MODE, PASS>; fp32: ffn_gemm_f32_kernel<MODE, PASS>
+    m = re.search(r"ffn_gemm(16|_f32)_kernel<(\d+), (\d+)>", name)
     if m:
-        return PASS_NAMES[int(m.group(2))]
-    m = re.search(r"ffn_gemm_kernel<([^,]+), (\d+), (\d+)>", name)
-    if m:
-        return PASS_NAMES[int(m.group(3))] + ("" if "short" in m.group(1) else "_f32")
+        return PASS_NAMES[int(m.group(3))] + ("_f32" if m.group(1) == "_f32" else "")
     m = re.search(r"moe::(?:\(anonymous namespace\)::)?(\w+)(<[^(]*>)?", name)
     if m:
         targs = (m.group(2) or "").replace("unsigned short", "bf16").replace("float", "f32")
