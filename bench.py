@@ -71,6 +71,9 @@ def parse():
                          "of mini-batches, drops vs average capacity factor for static "
                          "capacities and for launch-frontier policies")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step in a HIP graph and time its replays (per-kernel "
+                         "times then come from as many instrumented eager steps)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead of the layer: time a plain device-to-device copy of this "
                          "many GiB (achievable HBM bandwidth; byte-counter calibration)")
@@ -394,17 +397,41 @@ def main():
     active = int((L.dest_row >= 0).any(dim=1).sum().item())
     status = int(L.status.item())
 
+    graph = None
+    if args.graph:
+        if variant in ("cached", "policy"):
+            raise SystemExit(f"--graph does not apply to --variant {variant} (host work per step)")
+        log("capturing one step")
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()                   # a step on the capture stream before capturing
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+
+    def timed(run, instrument):
+        B.moe_timing_enable(instrument)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        B.moe_timing_enable(False)
+        return e0.elapsed_time(e1)
+
     B.moe_timing_report()            # drop warmup records
-    B.moe_timing_enable(True)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record()
-    for _ in range(args.steps):
-        step()
-    ev1.record()
-    torch.cuda.synchronize()
-    B.moe_timing_enable(False)
-    total_ms = ev0.elapsed_time(ev1)
+    if graph is None:
+        total_ms = timed(step, True)
+        kern_ms = total_ms
+    else:
+        total_ms = timed(graph.replay, False)
+        kern_ms = timed(step, True)  # per-kernel times: instrumented eager steps
     kern = B.moe_timing_report()
     ms_step = total_ms / args.steps
 
@@ -416,7 +443,7 @@ def main():
     detail = {}
     for name, (n, ms) in kern.items():
         avg = ms / max(n, 1)
-        row = {"launches": n, "avg_ms": round(avg, 4), "share": round(ms / total_ms, 4)}
+        row = {"launches": n, "avg_ms": round(avg, 4), "share": round(ms / kern_ms, 4)}
         if name in fl:
             row["tflops"] = round(fl_alg[name] / avg / 1e9, 1)
             row["frac_mfma_peak"] = round(fl_alg[name] / avg / 1e9 / peak, 4)
@@ -471,9 +498,13 @@ def main():
         "cpu_baseline": cpu,
         "detail": {"kept_rows": kept, "executed_rows": executed, "status": status,
                    "gemm_tflops": round(gemm_fl / (gemm_ms / 1e3) / 1e12, 1) if gemm_ms else None,
-                   "gemm_share": round(gemm_ms / total_ms, 4),
+                   "gemm_share": round(gemm_ms / kern_ms, 4),
                    "input_gen_s": round(t_gen, 1), "kernels": detail},
     }
+    if graph is not None:
+        out["config"]["launch"] = "HIP graph replay of one captured step"
+        out["detail"]["kernel_timing"] = (f"{args.steps} instrumented eager steps after the "
+                                          f"timed replays ({kern_ms / args.steps:.4f} ms/step)")
     if variant != "base":
         out["config"]["variant"] = variant
     if variant == "balance":
