@@ -119,6 +119,22 @@ __global__ __launch_bounds__(256) void route_hist_kernel(
   if (threadIdx.x < E) hist[static_cast<size_t>(blockIdx.x) * E + threadIdx.x] = h[threadIdx.x];
 }
 
+// Usable rows of expert e's region: its capacity, clamped to the region the
+// offsets give it and to rows_alloc (0 for a region starting out of range).
+__device__ __forceinline__ int64_t region_room(const int32_t* __restrict__ capacity,
+                                               const int32_t* __restrict__ offsets,
+                                               int64_t rows_alloc, int e) {
+  const int64_t off = offsets[e];
+  int64_t room = 0;
+  if (off >= 0) {
+    room = capacity[e];
+    room = min(room, static_cast<int64_t>(offsets[e + 1]) - off);
+    room = min(room, rows_alloc - off);
+    room = max(room, int64_t(0));
+  }
+  return room;
+}
+
 // Dispatch step 2: per-expert exclusive scan over chunks, counts, the usable
 // capacity of each region, fill.
 __global__ __launch_bounds__(64) void route_scan_kernel(
@@ -145,35 +161,66 @@ __global__ __launch_bounds__(64) void route_scan_kernel(
     run += hist[static_cast<size_t>(b) * E + e];
   }
   counts[e] = run;
-  const int64_t off = offsets[e];
-  const int64_t cap = capacity[e];
-  int64_t room = 0;
-  if (off >= 0) {
-    room = cap;
-    room = min(room, static_cast<int64_t>(offsets[e + 1]) - off);
-    room = min(room, rows_alloc - off);
-    room = max(room, int64_t(0));
-  }
-  if (room < cap) atomicOr(status, MOE_STATUS_REGION);
+  const int64_t room = region_room(capacity, offsets, rows_alloc, e);
+  if (room < capacity[e]) atomicOr(status, MOE_STATUS_REGION);
   cap_eff[e] = static_cast<int32_t>(room);
   fill[e] = static_cast<int32_t>(min(static_cast<int64_t>(run), room));
 }
 
 // Dispatch step 3: rank within chunk (wavefront ballots), keep/dest/src.
+// SCAN: small batches (at most kScanChunks chunks) skip step 2; every
+// workgroup sums the histograms of the chunks before its own, and workgroup
+// 0 writes counts, fill and the region status bit.
+constexpr int kScanChunks = 64;
+template <bool SCAN>
 __global__ __launch_bounds__(256) void route_rank_kernel(
     const int32_t* __restrict__ ids, int T, int E, int k, const int32_t* __restrict__ base,
     const int32_t* __restrict__ cap_eff, const int32_t* __restrict__ offsets,
-    int32_t* __restrict__ dest_row, int32_t* __restrict__ src) {
+    int32_t* __restrict__ dest_row, int32_t* __restrict__ src,
+    const int32_t* __restrict__ hist, int nblk, const int32_t* __restrict__ capacity,
+    int64_t rows_alloc, int32_t* __restrict__ counts, int32_t* __restrict__ fill,
+    int32_t* status) {
   __shared__ int run[kMaxE];
   __shared__ int wcnt[4][kMaxE];
   __shared__ int capv[kMaxE];
   __shared__ int offv[kMaxE];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (threadIdx.x < E) {
-    run[threadIdx.x] = base[static_cast<size_t>(blockIdx.x) * E + threadIdx.x];
-    capv[threadIdx.x] = cap_eff[threadIdx.x];
-    offv[threadIdx.x] = offsets[threadIdx.x];
+  if constexpr (SCAN) {
+    // wave w sums chunks w, w + 4, ...: those before this one (wcnt) and
+    // all of them (tot)
+    __shared__ int tot[4][kMaxE];
+    if (lane < E) {
+      int lo = 0, all = 0;
+      for (int b = wave; b < nblk; b += 4) {
+        const int v = hist[static_cast<size_t>(b) * E + lane];
+        all += v;
+        lo += b < static_cast<int>(blockIdx.x) ? v : 0;
+      }
+      wcnt[wave][lane] = lo;
+      tot[wave][lane] = all;
+    }
+    __syncthreads();
+    if (threadIdx.x < E) {
+      const int e = threadIdx.x;
+      run[e] = wcnt[0][e] + wcnt[1][e] + wcnt[2][e] + wcnt[3][e];
+      const int total = tot[0][e] + tot[1][e] + tot[2][e] + tot[3][e];
+      const int64_t room = region_room(capacity, offsets, rows_alloc, e);
+      if (blockIdx.x == 0) {
+        counts[e] = total;
+        fill[e] = static_cast<int32_t>(min(static_cast<int64_t>(total), room));
+        if (room < capacity[e]) atomicOr(status, MOE_STATUS_REGION);
+      }
+      capv[e] = static_cast<int32_t>(room);
+      offv[e] = offsets[e];
+    }
+  } else {
+    if (threadIdx.x < E) {
+      run[threadIdx.x] = base[static_cast<size_t>(blockIdx.x) * E + threadIdx.x];
+      capv[threadIdx.x] = cap_eff[threadIdx.x];
+      offv[threadIdx.x] = offsets[threadIdx.x];
+    }
   }
+  __syncthreads();
   for (int i = threadIdx.x; i < 4 * kMaxE; i += 256) (&wcnt[0][0])[i] = 0;
   __syncthreads();
   const int64_t n = static_cast<int64_t>(T) * k;
@@ -493,18 +540,27 @@ extern "C" moe_status moe_dispatch(void* stream, moe_dtype dt, int T, int d, int
     route_hist_kernel<<<nblk, 256, 0, s>>>(ids, T, E, k, nblk, rows_alloc, hist, src, status);
     MOE_LAUNCH_CHECK();
   }
-  {
-    MOE_TIMED("route_scan", s);
-    route_scan_kernel<<<1, 64, 0, s>>>(hist, nblk, E, capacity, offsets, rows_alloc, base,
-                                       cap_eff, counts, fill, status);
+  if (nblk <= kScanChunks) {
+    // the rank kernel does the scan too (and writes counts and fill)
+    MOE_TIMED("route_rank", s);
+    route_rank_kernel<true><<<nblk, 256, 0, s>>>(ids, T, E, k, nullptr, nullptr, offsets,
+                                                 dest_row, src, hist, nblk, capacity,
+                                                 rows_alloc, counts, fill, status);
+    MOE_LAUNCH_CHECK();
+  } else {
+    {
+      MOE_TIMED("route_scan", s);
+      route_scan_kernel<<<1, 64, 0, s>>>(hist, nblk, E, capacity, offsets, rows_alloc, base,
+                                         cap_eff, counts, fill, status);
+      MOE_LAUNCH_CHECK();
+    }
+    MOE_TIMED("route_rank", s);
+    route_rank_kernel<false><<<nblk, 256, 0, s>>>(ids, T, E, k, base, cap_eff, offsets,
+                                                  dest_row, src, nullptr, nblk, nullptr,
+                                                  rows_alloc, nullptr, nullptr, nullptr);
     MOE_LAUNCH_CHECK();
   }
   if (T == 0) return MOE_OK;
-  {
-    MOE_TIMED("route_rank", s);
-    route_rank_kernel<<<nblk, 256, 0, s>>>(ids, T, E, k, base, cap_eff, offsets, dest_row, src);
-    MOE_LAUNCH_CHECK();
-  }
   MOE_TIMED("dispatch_gather", s);
   const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
   gather_rows_kernel<<<nblocks(T, kRowWaves), 256, 0, s>>>(
