@@ -159,9 +159,12 @@ def _bf16_rows(T, d, seed):
     return W.to_bf16_bits(np.random.default_rng(seed).standard_normal((T, d)).astype(np.float32))
 
 
+# T*k = 65536 is the largest batch whose rank kernel also does the per-expert
+# scan (64 chunks of 1024 assignments); 65538 takes the separate scan launch
 @pytest.mark.parametrize("T,E,k,cap_kind", [
     (5000, 8, 2, "static"), (5000, 8, 2, "dynamic"), (777, 64, 1, "tight"),
-    (4096, 5, 3, "zero_some"), (3, 4, 2, "tight"), (9000, 32, 2, "exact")])
+    (4096, 5, 3, "zero_some"), (3, 4, 2, "tight"), (9000, 32, 2, "exact"),
+    (32768, 16, 2, "tight"), (32769, 16, 2, "tight")])
 def test_dispatch_random_ids(T, E, k, cap_kind):
     rng = np.random.default_rng(T * 7 + E)
     ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
@@ -193,14 +196,15 @@ def test_dispatch_cached_zipf_ids_fp32_rows():
     assert (g["dest_row"] >= 0).all()
 
 
-def test_dispatch_faults_and_region_overflow():
+@pytest.mark.parametrize("T", [4500, 33000])   # scan in the rank kernel / its own launch
+def test_dispatch_faults_and_region_overflow(T):
     rng = np.random.default_rng(9)
-    T, E, k = 4500, 6, 2
+    E, k = 6, 2
     ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
     ids[10, 0] = 99
     ids[11, 1] = -5
-    ids[4400, 1] = ids[4400, 0]
-    cap = np.full(E, 900)
+    ids[T - 100, 1] = ids[T - 100, 0]
+    cap = np.full(E, T // 5)
     off = O.exclusive_offsets(cap)
     rows_alloc = int(off[-1]) - 1000                  # the last region does not fit
     g, s = _check_dispatch(_bf16_rows(T, 16, 3), ids, E, cap, off, rows_alloc)
