@@ -192,7 +192,7 @@ def policy_sweep(args):
     """Drops vs average capacity factor over a drifting trajectory of
     mini-batches (routing only: count -> capacity -> dispatch of narrow
     rows), for static capacities (Eq. 4) and launch-frontier policies
-    (Section 3.1 with the recompile appendix).  The demand per mini-batch is
+    (Section 4.1 with the recompile appendix).  The demand per mini-batch is
     the library's own count; the capacity trajectories of these settings are
     checked against the oracle in the GPU tests, not here."""
     import numpy as np

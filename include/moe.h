@@ -4,8 +4,8 @@
  * capacities and a cached-assignment (gate bypass) path, forward and
  * backward.  Method: Kossmann, Jia, Aiken, "Optimizing Mixture of Experts
  * using Dynamic Recompilations" (MLSys 2022): Algorithm 1 (top-k MoE
- * forward), Eq. 1 (weighted sum of expert outputs), Eq. 4 and Section 3.1
- * (expert capacity, drops, dynamic capacity factors), Section 3.2 (sample
+ * forward), Eq. 1 (weighted sum of expert outputs), Eq. 4 and Section 4.1
+ * (expert capacity, drops, dynamic capacity factors), Section 4.2 (sample
  * assignment caching), Eq. 3 (balance term), Eq. 2 and its appendix
  * (specification loss, AggregateSpec), Section 3 with its implementation
  * appendix (metric-driven changes at the launch frontier).
@@ -92,7 +92,7 @@ moe_status moe_gate_topk(void* stream, moe_dtype dt, int T, int d, int E, int k,
 
 /*
  * moe_count - the per-expert load that dynamic capacity factors follow
- * (Section 3.1: how many samples the gate assigns to each expert), before
+ * (Section 4.1: how many samples the gate assigns to each expert), before
  * any capacity is applied.
  *   ids    [T,k] int32 expert ids (gate output or cached)
  *   counts [E]   int32 out: live assignments per expert.  An id outside
@@ -105,7 +105,7 @@ moe_status moe_count(void* stream, int T, int E, int k, const int32_t* ids,
                      int32_t* counts, int32_t* status);
 
 /*
- * moe_update_capacity - Eq. 4 and Section 3.1: per-expert capacities and
+ * moe_update_capacity - Eq. 4 and Section 4.1: per-expert capacities and
  * the row layout of the grouped expert buffer.
  *   counts == NULL: static capacity factor alpha = num/den,
  *                   C_e = ceil(num*T*k / (den*E)) for every expert;
@@ -129,13 +129,13 @@ moe_status moe_update_capacity(void* stream, int T, int k, int E,
 size_t moe_dispatch_workspace_bytes(int T, int E, int k);
 
 /*
- * moe_dispatch - GroupBy with the capacity/drop rule of Section 3.1: each
+ * moe_dispatch - GroupBy with the capacity/drop rule of Section 4.1: each
  * expert's tensor is filled from its first entry, assignments beyond the
  * expert's capacity are dropped.  Priority: all first choices in token
  * order, then all second choices, and so on.
  *   x         [T,d]          layer dtype
  *   ids       [T,k]          int32 expert ids (gate output or cached ids:
- *                            the gate-bypass path of Section 3.2)
+ *                            the gate-bypass path of Section 4.2)
  *   capacity  [E], offsets [E+1]  as written by moe_update_capacity
  *   rows_alloc                rows of the grouped buffers
  *   counts    [E]   out: live assignments per expert (as moe_count)
@@ -165,7 +165,7 @@ size_t moe_ffn_bwd_workspace_bytes(moe_dtype dt, moe_act act, int E, int d,
 
 /*
  * moe_expert_ffn_fwd - the expert modules E_e(x) of Algorithm 1, run on each
- * expert's own rows only (dynamically sized expert tensors, Section 3.1).
+ * expert's own rows only (dynamically sized expert tensors, Section 4.1).
  * For expert e the rows are [offsets[e], offsets[e]+rows[e]) of the grouped
  * buffers; rows[e] is clamped to the expert's region and to rows_alloc.
  *   MOE_RELU / MOE_GELU_TANH: H = X w1_e^T, A = act(H), Y = A w2_e^T
@@ -203,7 +203,7 @@ moe_status moe_combine(void* stream, moe_dtype dt, int T, int d, int k,
 
 /*
  * moe_combine_bwd - backward of moe_combine.  Dropped assignments get zero
- * gradient (Section 3.1).
+ * gradient (Section 4.1).
  *   dy       [T,d] upstream gradient
  *   dweights [T,k] f32 out: <dy[t], y_disp[dest_row[t,j]]> if kept, else 0
  *   dy_disp  [rows_alloc,d] out: dy_disp[dest_row[t,j]] = weights[t,j]*dy[t]
@@ -330,7 +330,7 @@ moe_status moe_spec_loss(void* stream, moe_dtype dt, int T, int d, int k,
                          int64_t rows_alloc, void* dy_disp, float* dweights,
                          float* loss, void* workspace, size_t workspace_bytes);
 
-/* ---- sample assignment caching (Section 3.2) ------------------------------ */
+/* ---- sample assignment caching (Section 4.2) ------------------------------ */
 
 /*
  * moe_cache_update - the Cache operator on one mini-batch: counts the
@@ -363,7 +363,7 @@ moe_status moe_cached_weights(void* stream, int T, int E, int k, int renorm,
                               float* weights);
 
 /*
- * moe_caching_decision - the caching switch with hysteresis of Section 5.2:
+ * moe_caching_decision - the caching switch with hysteresis of Section 5.3:
  * off -> on when unchanged/samples >= on_num/on_den and epoch >= min_epoch;
  * on -> off when unchanged/samples < off_num/off_den (exact integer
  * comparison).  The paper's setting is 96/100, 90/100, epoch 10.  Returns
@@ -375,7 +375,7 @@ int moe_caching_decision(int enabled, int64_t unchanged, int64_t samples,
                          int epoch, int on_num, int on_den, int off_num,
                          int off_den, int min_epoch);
 
-/* ---- capacity policy at the launch frontier (Section 3, Section 3.1) ------ */
+/* ---- capacity policy at the launch frontier (Section 3, Section 4.1) ------ */
 
 /*
  * A host object that turns the per-expert assignment counts of past

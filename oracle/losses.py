@@ -20,7 +20,7 @@ S1 L is the mean squared error over the d features of one prediction,
    tokens of Eq. 2's per-sample sum.
 S2 The sum in Eq. 2 runs over the chosen experts whose assignment was kept;
    a dropped assignment has no prediction, contributes nothing and gets no
-   gradient (as in the forward pass, Section 3.1).  Its AggregateSpec row
+   gradient (as in the forward pass, Section 4.1).  Its AggregateSpec row
    is zero.
 S3 g_i is the combine weight of the choice (Algorithm 1's normalised score),
    the same value the cooperation loss's weighted sum uses.

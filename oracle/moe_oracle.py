@@ -8,12 +8,12 @@ Paper passages followed (Kossmann, Jia, Aiken, MLSys 2022):
   normalised weights of the picks, weighted sum of the picked experts.
 * Eq. 1 (cooperation loss): the layer output is the gate-weighted sum of
   expert outputs.
-* Section 3.1 (dynamic capacity factors) with Eq. 4: capacity
+* Section 4.1 (dynamic capacity factors) with Eq. 4: capacity
   C = alpha * batch * k / n, samples beyond an expert's capacity are dropped
   (no forward contribution, zero gradient), the first entries of an expert's
   tensor are the ones filled; the per-expert assigned-sample count is the
   model metric that dynamic capacities are derived from.
-* Section 3.2 (sample assignment caching): previously computed assignments
+* Section 4.2 (sample assignment caching): previously computed assignments
   replace the gate's output when building the expert batches.
 
 Precision: every step is evaluated in float64.  For a bf16 layer the values
@@ -150,7 +150,7 @@ def gate_weights(p: np.ndarray, ids: np.ndarray, renorm: int) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
-# per-expert load (the Section 3.1 model metric) and capacities (Eq. 4)
+# per-expert load (the Section 4.1 model metric) and capacities (Eq. 4)
 # ----------------------------------------------------------------------------
 def validate_assignments(ids: np.ndarray, E: int) -> Tuple[np.ndarray, int]:
     """Which (t, j) assignments are live, and the status bits.
@@ -172,7 +172,7 @@ def validate_assignments(ids: np.ndarray, E: int) -> Tuple[np.ndarray, int]:
 
 def count_assignments(ids: np.ndarray, E: int) -> np.ndarray:
     """counts[e] = number of live assignments to expert e, before capacity:
-    how many samples the gate assigns to each expert (Section 3.1)."""
+    how many samples the gate assigns to each expert (Section 4.1)."""
     live, _ = validate_assignments(ids, E)
     return np.bincount(np.asarray(ids)[live].astype(np.int64), minlength=E).astype(np.int64)
 
@@ -193,7 +193,7 @@ def capacity_static(T: int, k: int, E: int, num: int, den: int,
 
 def capacity_dynamic(counts: np.ndarray, T: int, num: int, den: int,
                      cap_min: int = 0) -> np.ndarray:
-    """Dynamic capacity factors (Section 3.1): each expert's capacity follows
+    """Dynamic capacity factors (Section 4.1): each expert's capacity follows
     its own observed load, C_e = ceil(num/den * counts[e]) in exact integer
     arithmetic, clamped to [cap_min, T].  num/den = 1 gives exact capacity."""
     out = np.empty(len(counts), dtype=np.int64)
@@ -211,14 +211,14 @@ def exclusive_offsets(capacity: np.ndarray) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
-# slot assignment and dispatch (GroupBy; Section 3.1 drop rule)
+# slot assignment and dispatch (GroupBy; Section 4.1 drop rule)
 # ----------------------------------------------------------------------------
 def assign_slots(ids: np.ndarray, E: int, capacity: np.ndarray,
                  offsets: np.ndarray, rows_alloc: int) -> Dict[str, np.ndarray]:
     """Place every live assignment in its expert's tensor.
 
     Expert e owns rows [offsets[e], offsets[e] + C_e) of the grouped buffer.
-    The buffer is filled from its first entry (Section 3.1); priority is
+    The buffer is filled from its first entry (Section 4.1); priority is
     all first choices in token order, then all second choices, ... (R4).
     An assignment whose position is >= C_e is dropped (dest_row = -1).
     A capacity region that overlaps the next expert's or runs past rows_alloc

@@ -2,16 +2,16 @@
 them.  TEST INFRASTRUCTURE ONLY (see the package docstring): nothing in the
 product path imports this module.
 
-* Section 3.2 (sample assignment caching): the Cache operator's metric, the
+* Section 4.2 (sample assignment caching): the Cache operator's metric, the
   number of samples whose assignment did not change since the cached one,
   and the cache update that stores the fresh assignment for the next epoch.
-* Section 5.2 (caching results): caching is switched on once at least 96% of
+* Section 5.3 (caching results): caching is switched on once at least 96% of
   the samples are correctly cached and not before epoch 10, and switched off
   when that share falls below 90%.
 * Section 3 (the recompile mechanism) with its implementation appendix:
   a model metric produced at the execution frontier drives a user trigger
   that alters the graph at the launch frontier, Delta_launch iterations
-  later; Section 3.1 applies it to per-expert capacities computed from the
+  later; Section 4.1 applies it to per-expert capacities computed from the
   observed per-expert assignment counts.
 
 Readings taken here (each also stated where it is used):
@@ -63,7 +63,7 @@ def cache_update(fresh_ids: np.ndarray, cache: np.ndarray) -> Tuple[int, np.ndar
 def caching_decision(enabled: bool, unchanged: int, samples: int, epoch: int,
                      on: Tuple[int, int] = (96, 100), off: Tuple[int, int] = (90, 100),
                      min_epoch: int = 10) -> bool:
-    """Hysteresis of Section 5.2 (C2): switch on at unchanged/samples >= on
+    """Hysteresis of Section 5.3 (C2): switch on at unchanged/samples >= on
     once epoch >= min_epoch, switch off at unchanged/samples < off."""
     if samples <= 0:
         return enabled

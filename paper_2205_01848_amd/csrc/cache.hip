@@ -1,4 +1,4 @@
-// Sample assignment caching (Section 3.2).
+// Sample assignment caching (Section 4.2).
 //
 // The Cache operator compares the gate's fresh picks of a mini-batch with
 // the picks cached for the same samples in the previous epoch, counts the
@@ -7,7 +7,7 @@
 // next epoch.  With caching on, the expert batches are built from the cached
 // picks while the gate runs; the combine weights are then the gate's fresh
 // probabilities read at the cached picks (moe_cached_weights).  The on/off
-// decision with hysteresis (Section 5.2: on at >= 96% correctly cached and
+// decision with hysteresis (Section 5.3: on at >= 96% correctly cached and
 // not before epoch 10, off below 90%) is a host function.
 
 #include "common.hpp"

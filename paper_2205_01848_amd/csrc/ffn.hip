@@ -1,5 +1,5 @@
 // Expert FFN of the MoE layer (the expert modules E_e of Algorithm 1) on
-// dynamically sized per-expert tensors (Section 3.1), forward and backward.
+// dynamically sized per-expert tensors (Section 4.1), forward and backward.
 //
 // Every product is one persistent grouped GEMM kernel in "NT" form,
 //     C[m, n] = sum_k A[m, k] * B[n, k]     (both operands K-contiguous),

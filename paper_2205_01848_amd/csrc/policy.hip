@@ -1,5 +1,5 @@
 // Host capacity policy driven by a model metric, applied at the launch
-// frontier (Section 3 and its implementation appendix; Section 3.1 for the
+// frontier (Section 3 and its implementation appendix; Section 4.1 for the
 // per-expert capacities).
 //
 // Every iteration the caller brackets its launches with moe_policy_begin and

@@ -1,5 +1,5 @@
 // Load counting, capacities, slot assignment + dispatch (GroupBy with the
-// Section 3.1 capacity/drop rule), combine (Aggregate) and their backward.
+// Section 4.1 capacity/drop rule), combine (Aggregate) and their backward.
 //
 // Slot assignment is a stable counting sort of the T*k assignments in
 // priority order q = j*T + t (all first choices in token order, then all

@@ -206,7 +206,7 @@ class MoELayer:
 
     def forward_cached(self, x, w1, w3, w2, *, cached, cache_out, unchanged, w_g, bias=None,
                        renorm=0, capacity=("dynamic", 1, 1), gate_stream=None, rows="fill"):
-        """Forward with sample assignment caching on (Section 3.2): the expert
+        """Forward with sample assignment caching on (Section 4.2): the expert
         batches are built from the cached picks while the gate runs on
         gate_stream; the combine waits for the gate and weighs the cached
         picks with the fresh probabilities.  The Cache operator counts the

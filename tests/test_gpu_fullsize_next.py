@@ -8,7 +8,7 @@ configuration bench.py's variants time:
   choice) rows against the oracle's expert rows, dweights and dy_disp rows of
   sampled tokens, and the loss against the sum the kernel's own dweights
   imply (a property that holds at any size);
-* caching (Section 3.2): the unchanged-sample count over all tokens, the
+* caching (Section 4.2): the unchanged-sample count over all tokens, the
   weights at cached picks, and sampled layer outputs with the gate on a
   second stream;
 * the capacity policy on device counts of c5-sized mini-batches.

@@ -4,7 +4,7 @@ path, against the CPU oracle on the same seeded inputs:
 * Eq. 3 balance term and its gradient through the gate backward;
 * AggregateSpec and the Eq. 2 specification loss with its gradients, alone
   and inside the layer backward;
-* the Cache operator (Section 3.2): unchanged-sample count and cache update,
+* the Cache operator (Section 4.2): unchanged-sample count and cache update,
   combine weights at cached picks, and the layer forward with the gate on a
   second stream;
 * the capacity policy at the launch frontier (Section 3 and its
@@ -194,7 +194,7 @@ def test_layer_backward_with_spec_loss_and_balance(name, lam):
     assert_close(to_np(L.dx), bw["dx"], rt, "dx")
 
 
-# ---- Section 3.2: sample assignment caching ------------------------------------------
+# ---- Section 4.2: sample assignment caching ------------------------------------------
 @pytest.mark.parametrize("T,E,k,frac", [(3000, 16, 2, 0.1), (70001, 64, 1, 0.03),
                                         (999, 8, 4, 0.5)])
 def test_cache_update_counts_and_stores(T, E, k, frac):

@@ -1,6 +1,6 @@
 """Host-side C functions of the library against the oracle, on the CPU (no
-device work): the caching decision with hysteresis (Section 5.2) and the
-capacity trigger (Section 3.1 with the recompile implementation appendix),
+device work): the caching decision with hysteresis (Section 5.3) and the
+capacity trigger (Section 4.1 with the recompile implementation appendix),
 bit-exact on the golden fixtures and on random inputs."""
 import json
 import os

@@ -1,5 +1,5 @@
-"""Pins of the oracle's cache metric (Section 3.2), caching hysteresis
-(Section 5.2) and launch-frontier capacity policy (Section 3.1 with the
+"""Pins of the oracle's cache metric (Section 4.2), caching hysteresis
+(Section 5.3) and launch-frontier capacity policy (Section 4.1 with the
 recompile implementation appendix): hand-worked fixtures under
 tests/golden/, brute force and closed forms."""
 import itertools

@@ -1,5 +1,5 @@
 """Pins of the oracle's capacity rule (Eq. 4, dynamic capacity factors) and
-slot assignment / drop rule (Section 3.1) against exact rationals, the
+slot assignment / drop rule (Section 4.1) against exact rationals, the
 quadratic brute-force definition and invariants."""
 import math
 from fractions import Fraction
@@ -171,7 +171,7 @@ def test_dispatch_is_exact_copy():
 
 def test_hand_worked_example():
     """A six-token, three-expert, top-2 batch worked out by hand from Eq. 4 and
-    the Section 3.1 rule (first entries of each expert tensor kept; priority:
+    the Section 4.1 rule (first entries of each expert tensor kept; priority:
     first choices in token order, then second choices).
 
     ids: t0 (0,1) t1 (0,2) t2 (1,0) t3 (0,1) t4 (2,0) t5 (0,2)
