@@ -191,6 +191,24 @@ moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act, int E,
                               size_t workspace_bytes);
 
 /*
+ * moe_zero_pad_rows - the padded static-shape baseline that Section 4.1
+ * compares against: an expert tensor of fixed capacity whose first entries
+ * hold the expert's samples and whose unused entries are zero, so they add
+ * nothing to the weight gradients.  Writes zeros to rows
+ * [offsets[e] + fill[e], offsets[e] + rows[e]) of buf for every expert,
+ * with rows[e] clamped to the expert's region and to rows_alloc as the FFN
+ * calls clamp it (fill[e] clamped to [0, rows[e]]).  Call it on x_disp after
+ * moe_dispatch and on dy_disp after moe_combine_bwd (or moe_spec_loss)
+ * before running the FFN with rows = capacity; the method itself
+ * (rows = fill) never reads those rows and does not need it.
+ *   offsets [E+1], fill [E], rows [E] int32
+ *   buf     [rows_alloc,d] layer dtype, in/out; other rows untouched
+ */
+moe_status moe_zero_pad_rows(void* stream, moe_dtype dt, int E, int d,
+                             const int32_t* offsets, const int32_t* fill,
+                             const int32_t* rows, int64_t rows_alloc, void* buf);
+
+/*
  * moe_combine - Aggregate (Algorithm 1's weighted sum, Eq. 1):
  * y[t] = sum over kept j, in order j = 0..k-1, of weights[t,j] *
  * y_disp[dest_row[t,j]], summed in float32 and rounded once.  A token with

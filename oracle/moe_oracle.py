@@ -142,11 +142,22 @@ def gate_weights(p: np.ndarray, ids: np.ndarray, renorm: int) -> np.ndarray:
     """normalize(score[indices]) of Algorithm 1 (reading R1): with renorm the
     picked probabilities are divided by their sum, else the raw probability
     of each pick is its weight.  Weights are fixed before capacity, so a drop
-    never re-normalises the survivors.  Returned as float32 values."""
-    sel = np.take_along_axis(p, ids.astype(np.int64), axis=1)
+    never re-normalises the survivors.  On the cached path (Section 4.2) an id
+    outside [0, E) is not a pick: its weight is 0 and it is left out of the
+    sum (the gate never produces one).  Returned as float32 values."""
+    sel = _picked_probs(p, ids)
     if renorm:
-        sel = sel / sel.sum(axis=1, keepdims=True)
+        tot = sel.sum(axis=1, keepdims=True)
+        sel = np.divide(sel, tot, out=np.zeros_like(sel), where=tot > 0)
     return _f32(sel)
+
+
+def _picked_probs(p: np.ndarray, ids: np.ndarray) -> np.ndarray:
+    """p[t, ids[t,j]], and 0 where ids[t,j] is not an expert index."""
+    idx = np.asarray(ids).astype(np.int64)
+    ok = (idx >= 0) & (idx < p.shape[1])
+    sel = np.take_along_axis(p, np.where(ok, idx, 0), axis=1)
+    return np.where(ok, sel, 0.0)
 
 
 # ----------------------------------------------------------------------------
@@ -494,17 +505,20 @@ def gate_bwd(logits: np.ndarray, ids: np.ndarray, dweights: np.ndarray,
     p = softmax(logits)
     T, E = p.shape
     idx = ids.astype(np.int64)
-    sel = np.take_along_axis(p, idx, axis=1)
+    ok = (idx >= 0) & (idx < E)          # an id outside [0, E) is no pick
+    sel = _picked_probs(p, idx)
     dw = np.asarray(dweights, dtype=np.float64)
     if renorm:
         S = sel.sum(axis=1, keepdims=True)
-        w = sel / S
-        g = (dw - (dw * w).sum(axis=1, keepdims=True)) / S
+        w = np.divide(sel, S, out=np.zeros_like(sel), where=S > 0)
+        g = np.divide(dw - (dw * w).sum(axis=1, keepdims=True), S,
+                      out=np.zeros_like(sel), where=S > 0)
     else:
         g = dw
     dp = np.zeros((T, E))
     for j in range(idx.shape[1]):
-        dp[np.arange(T), idx[:, j]] += g[:, j]
+        rows = np.nonzero(ok[:, j])[0]
+        dp[rows, idx[rows, j]] += g[rows, j]
     if dprob_coef is not None:
         dp += np.asarray(dprob_coef, dtype=np.float64)[None, :]
     dl = p * (dp - (dp * p).sum(axis=1, keepdims=True))

@@ -37,6 +37,7 @@ SIGNATURES = {
     "moe_ffn_bwd_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_i64]),
     "moe_expert_ffn_fwd": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_int, _p, _p,
                                     _c_i64, _p, _p, _p, _p, _p, _p, _p, _c_size]),
+    "moe_zero_pad_rows": (_c_int, [_p, _c_int, _c_int, _c_int, _p, _p, _p, _c_i64, _p]),
     "moe_combine": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_i64, _p, _p, _p, _p]),
     "moe_combine_bwd": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_i64, _p, _p, _p,
                                  _p, _p, _p]),
@@ -224,6 +225,16 @@ def moe_expert_ffn_fwd(act, offsets, rows, x_disp, w1, w3, w2, h_save, y_disp, w
                                     x_disp.shape[0], _ptr(x_disp), _ptr(w1), _ptr(w3), _ptr(w2),
                                     _ptr(h_save), _ptr(y_disp), _ptr(ws), _nbytes(ws)),
            "moe_expert_ffn_fwd")
+
+
+def moe_zero_pad_rows(offsets, fill, rows, buf):
+    E = fill.shape[0]
+    R, d = buf.shape
+    _need(offsets, E + 1, "offsets", _I32)
+    _need(fill, E, "fill", _I32)
+    _need(rows, E, "rows", _I32)
+    _check(lib().moe_zero_pad_rows(_stream(), _dt(buf), E, d, _ptr(offsets), _ptr(fill),
+                                   _ptr(rows), R, _ptr(buf)), "moe_zero_pad_rows")
 
 
 def moe_combine(y_disp, dest_row, weights, y):

@@ -277,19 +277,22 @@ __global__ __launch_bounds__(64) void gate_bwd_dlogits_kernel(
   }
   const int32_t* id = ids + static_cast<size_t>(t) * k;
   const float* dw = dweights + static_cast<size_t>(t) * k;
+  // An id outside [0, E) (a bad cached id) is not a pick: its weight is 0
+  // and it takes no part in the normalisation, as in moe_cached_weights.
   float S = 0.f, dot = 0.f;
   for (int j = 0; j < k; ++j) {
-    const int e = min(max(id[j], 0), E - 1);
-    S += sp[lane][e];
+    const int e = id[j];
+    if (e >= 0 && e < E) S += sp[lane][e];
   }
   if (renorm) {
     for (int j = 0; j < k; ++j) {
-      const int e = min(max(id[j], 0), E - 1);
-      dot += dw[j] * (sp[lane][e] / S);
+      const int e = id[j];
+      if (e >= 0 && e < E) dot += dw[j] * (sp[lane][e] / S);
     }
   }
   for (int j = 0; j < k; ++j) {
-    const int e = min(max(id[j], 0), E - 1);
+    const int e = id[j];
+    if (e < 0 || e >= E) continue;
     const float g = renorm ? (dw[j] - dot) / S : dw[j];
     sdp[lane][e] += g;
   }

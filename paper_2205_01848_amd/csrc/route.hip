@@ -469,6 +469,47 @@ __global__ __launch_bounds__(256) void dispatch_bwd_kernel(
   }
 }
 
+// Padded static baseline: zero rows [offsets[e] + fill[e], offsets[e] + rows[e])
+// of a grouped buffer, rows[e] clamped to the expert's region and to
+// rows_alloc exactly as the FFN schedule clamps it.  A wavefront takes one
+// row; lane e tests expert e's unfilled range and a ballot decides.
+constexpr int kPadRowsPerBlock = 16;
+
+__global__ __launch_bounds__(256) void zero_pad_rows_kernel(
+    const int32_t* __restrict__ offsets, const int32_t* __restrict__ fill,
+    const int32_t* __restrict__ rows, int E, int64_t rows_alloc, int nvec,
+    uint4* __restrict__ buf) {
+  __shared__ int64_t lo[kMaxE], hi[kMaxE];
+  if (threadIdx.x < kMaxE) {
+    const int e = threadIdx.x;
+    int64_t a = 0, b = 0;
+    if (e < E) {
+      const int64_t off = offsets[e];
+      int64_t m = rows[e];
+      if (off < 0 || off >= rows_alloc) m = 0;
+      m = min(m, static_cast<int64_t>(offsets[e + 1]) - off);
+      m = min(m, rows_alloc - off);
+      m = max(m, int64_t(0));
+      const int64_t fl = min(max(static_cast<int64_t>(fill[e]), int64_t(0)), m);
+      a = off + fl;
+      b = off + m;
+    }
+    lo[e] = a;
+    hi[e] = b;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  for (int i = wave; i < kPadRowsPerBlock; i += kRowWaves) {
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * kPadRowsPerBlock + i;
+    if (r >= rows_alloc) break;
+    const bool mine = lane < E && r >= lo[lane] && r < hi[lane];
+    if (__ballot(mine) == 0) continue;
+    uint4* row = buf + static_cast<size_t>(r) * nvec;
+    for (int v = lane; v < nvec; v += 64) row[v] = make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
 inline int nblocks(int64_t n, int per) { return static_cast<int>((n + per - 1) / per); }
 
 }  // namespace
@@ -651,6 +692,22 @@ extern "C" moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d,
   else if (k <= 2) go(std::integral_constant<int, 2>{});
   else if (k <= 4) go(std::integral_constant<int, 4>{});
   else go(std::integral_constant<int, 8>{});
+  MOE_LAUNCH_CHECK();
+  return MOE_OK;
+}
+
+extern "C" moe_status moe_zero_pad_rows(void* stream, moe_dtype dt, int E, int d,
+                                        const int32_t* offsets, const int32_t* fill,
+                                        const int32_t* rows, int64_t rows_alloc, void* buf) {
+  if (!dtype_ok(dt) || E < 1 || E > kMaxE || !width_ok(d) || !rows_ok(rows_alloc))
+    return MOE_EINVAL;
+  if (rows_alloc == 0) return MOE_OK;
+  if (!offsets || !fill || !rows || !buf || !aligned16(buf)) return MOE_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
+  MOE_TIMED("zero_pad_rows", s);
+  zero_pad_rows_kernel<<<nblocks(rows_alloc, kPadRowsPerBlock), 256, 0, s>>>(
+      offsets, fill, rows, E, rows_alloc, nvec, static_cast<uint4*>(buf));
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }

@@ -107,7 +107,14 @@ class MoELayer:
                        self.x_disp, self.status, self.ws_dispatch)
 
     def ffn_fwd(self, w1, w3, w2, rows: str = "fill"):
-        r = self.fill if rows == "fill" else self.capacity
+        """rows="fill": the method, each expert over its kept rows.
+        rows="capacity": the padded static-shape baseline, each expert over
+        its whole capacity with the unfilled rows of x_disp zeroed first."""
+        if rows == "fill":
+            r = self.fill
+        else:
+            r = self.capacity
+            B.moe_zero_pad_rows(self.offsets, self.fill, r, self.x_disp)
         B.moe_expert_ffn_fwd(self.act, self.offsets, r, self.x_disp, w1, w3, w2, self.h_save,
                              self.y_disp, self.ws_fwd)
 
@@ -153,7 +160,13 @@ class MoELayer:
                           self.dweights)
 
     def ffn_bwd(self, w1, w3, w2, rows: str = "fill"):
-        r = self.fill if rows == "fill" else self.capacity
+        """rows="capacity" zeroes the unfilled rows of dy_disp first, so the
+        padding adds nothing to the weight gradients."""
+        if rows == "fill":
+            r = self.fill
+        else:
+            r = self.capacity
+            B.moe_zero_pad_rows(self.offsets, self.fill, r, self.dy_disp)
         B.moe_expert_ffn_bwd(self.act, self.offsets, r, self.x_disp, self.h_save, w1, w3, w2,
                              self.dy_disp, self.dx_disp, self.dw1, self.dw3, self.dw2,
                              self.ws_bwd)
@@ -211,13 +224,16 @@ class MoELayer:
         gate_stream; the combine waits for the gate and weighs the cached
         picks with the fresh probabilities.  The Cache operator counts the
         samples whose picks did not change (added to `unchanged`) and writes
-        the fresh picks to cache_out, which must not be `cached` when the gate
-        runs on another stream.  Backward: ids=cached,
-        weights=self.cached_weights."""
+        the fresh picks to cache_out.  cache_out must not be `cached`: the
+        dispatch reads the cached picks after the gate (on either stream),
+        and the backward (ids=cached, weights=self.cached_weights) reads them
+        again, so storing the fresh picks over them would route one set of
+        picks and weigh or differentiate another."""
         main = torch.cuda.current_stream(self.dev)
         gs = gate_stream if gate_stream is not None else main
-        if gs is not main and cache_out.data_ptr() == cached.data_ptr():
-            raise ValueError("cache_out must differ from cached when the gate runs concurrently")
+        if cache_out.data_ptr() == cached.data_ptr():
+            raise ValueError("cache_out must be a different buffer from cached: the cached "
+                             "picks are read by the dispatch and the backward of this step")
         if self.cached_weights is None:
             self.cached_weights = torch.empty(self.T, self.k, dtype=torch.float32,
                                               device=self.dev)

@@ -221,3 +221,33 @@ def test_gate_backward(dt, E, k, renorm):
     dl_ref, dwg_ref = O.gate_bwd(logits, ids, dwts, renorm, _dec(x, dt))
     assert_close(to_np(dl), dl_ref, 1e-5, "dlogits")
     assert_close(to_np(dwg), dwg_ref, 1e-5, "dw_g")
+
+
+@pytest.mark.parametrize("renorm", [0, 1])
+def test_gate_backward_skips_invalid_cached_ids(renorm):
+    """Cached picks with ids outside [0, E): the gate backward leaves them out
+    of the normalisation, as moe_cached_weights does in the forward."""
+    rng = np.random.default_rng(71)
+    T, d, E, k = 700, 136, 8, 2
+    x = _enc(rng.standard_normal((T, d)), "bf16")
+    logits = (rng.standard_normal((T, E)) * 2).astype(np.float32)
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    ids[::5, 1] = E + 2
+    ids[3::11, 0] = -4
+    dwts = rng.standard_normal((T, k)).astype(np.float32)
+    dwts[ids >= E] = 0.0
+    dwts[ids < 0] = 0.0
+    t_ids = torch.from_numpy(ids).to(dev())
+    t_l = torch.from_numpy(logits).to(dev())
+    w = torch.empty(T, k, dtype=torch.float32, device=dev())
+    B.moe_cached_weights(t_l, t_ids, renorm, w)
+    dl = torch.empty(T, E, dtype=torch.float32, device=dev())
+    dwg = torch.empty(E, d, dtype=torch.float32, device=dev())
+    ws = B.workspace(B.moe_gate_bwd_workspace_bytes(T, d, E), dev())
+    B.moe_gate_bwd(to_dev(x, "bf16"), t_l, t_ids, torch.from_numpy(dwts).to(dev()), renorm, dl,
+                   dwg, ws)
+    torch.cuda.synchronize()
+    assert_close(to_np(w), O.gate_weights(O.softmax(logits), ids, renorm), 1e-6, "weights")
+    dl_ref, dwg_ref = O.gate_bwd(logits, ids, dwts, renorm, _dec(x, "bf16"))
+    assert_close(to_np(dl), dl_ref, 1e-5, "dlogits")
+    assert_close(to_np(dwg), dwg_ref, 1e-5, "dw_g")

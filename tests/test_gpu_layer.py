@@ -172,3 +172,60 @@ def test_lagged_dynamic_capacity_uses_previous_counts():
                          r2["weights"], cap, R, wl.E)
     np.testing.assert_array_equal(to_np(L.dest_row), fw["dest_row"])
     assert_close(to_np(L.y), fw["y"], 2e-2, "y")
+
+
+@pytest.mark.parametrize("act", ["relu", "swiglu"])
+def test_padded_static_baseline_weight_gradients_equal_method(act):
+    """The padded static-shape baseline (every expert over its whole static
+    capacity, rows = capacity) zeroes the unfilled rows of x_disp and dy_disp,
+    so its weight gradients equal the method's (rows = fill) bit for bit, and
+    y and dx agree.  Dyadic inputs and combine weights keep every sum exact,
+    so the differing split-K orders of the two runs cannot change a bit.  The
+    grouped buffers start as NaN, so an unzeroed row would show."""
+    rng = np.random.default_rng(81)
+    T, d, E, k, f = 900, 64, 4, 2, 128
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    ids[: T // 2, 0] = 0                      # skew: expert 0 overflows, others stay short
+    for t in range(T // 2):
+        if ids[t, 1] == 0:
+            ids[t, 1] = 1 + t % (E - 1)
+    wts = np.tile(np.array([0.75, 0.25], np.float32), (T, 1))
+    bf = lambda a: to_dev(W.to_bf16_bits(a.astype(np.float32)), "bf16")
+    x = bf(rng.integers(-2, 3, (T, d)) / 4.0)
+    dy = bf(rng.integers(-2, 3, (T, d)) / 4.0)
+    w1 = bf(rng.integers(-2, 3, (E, f, d)) / 16.0)
+    w3 = bf(rng.integers(-2, 3, (E, f, d)) / 16.0) if act == "swiglu" else None
+    w2 = bf(rng.integers(-2, 3, (E, d, f)) / 16.0)
+    t_ids, t_w = torch.from_numpy(ids).to(dev()), torch.from_numpy(wts).to(dev())
+    num, den = 1, 1                           # static alpha = 1: C = 450 per expert
+    R = rows_alloc_for("static", T, k, E, num, den)
+    out = {}
+    for rows in ("fill", "capacity"):
+        L = MoELayer(T, d, E, k, f, act, torch.bfloat16, R, backward=True, gate=False)
+        for buf in (L.x_disp, L.dy_disp):
+            buf.fill_(float("nan"))
+        L.forward(x, w1, w3, w2, ids=t_ids, weights=t_w, capacity=("static", num, den),
+                  rows=rows)
+        L.backward(x, dy, w1, w3, w2, weights=t_w, rows=rows)
+        torch.cuda.synchronize()
+        out[rows] = {n: getattr(L, n).clone() for n in ("y", "dx", "dw1", "dw2", "fill",
+                                                           "capacity", "dest_row")}
+        if act == "swiglu":
+            out[rows]["dw3"] = L.dw3.clone()
+    fill, cap = to_np(out["fill"]["fill"]), to_np(out["fill"]["capacity"])
+    assert (fill < cap).sum() >= 2 and (fill == cap).any()    # padding and overflow both occur
+    for n in out["fill"]:
+        assert torch.equal(out["fill"][n], out["capacity"][n]), n
+    assert torch.isfinite(out["capacity"]["dw1"]).all()
+    # and the method's gradients are the oracle's
+    X, DY = to_np(x), to_np(dy)
+    f64 = lambda t: None if t is None else to_np(t)
+    capo = O.capacity_static(T, k, E, num, den)
+    fw = O.layer_forward(X, f64(w1), f64(w3), f64(w2), act, "bf16", ids, wts.astype(np.float64),
+                         capo, R, E)
+    np.testing.assert_array_equal(to_np(out["fill"]["dest_row"]), fw["dest_row"])
+    bw = O.layer_backward(fw, X, DY, f64(w1), f64(w3), f64(w2), act, "bf16", ids,
+                          wts.astype(np.float64), E)
+    rt = RTOL["bf16"]
+    assert_close(to_np(out["capacity"]["dw1"]), bw["dW1"], rt, "dW1")
+    assert_close(to_np(out["capacity"]["dw2"]), bw["dW2"], rt, "dW2")

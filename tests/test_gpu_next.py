@@ -295,6 +295,27 @@ def test_forward_cached_with_concurrent_gate(concurrent):
     assert_close(to_np(L.dx), bw["dx"], rt, "dx")
 
 
+def test_forward_cached_rejects_cache_stored_in_place():
+    """The cached picks drive the dispatch and the backward of the same
+    step, so the fresh picks may not be stored over them, on one stream or
+    two."""
+    wl = scaled_small(W, "c5", T=256, d=64, f=64)
+    I = W.make_inputs(wl)
+    dt, T, E, k = "bf16", wl.T, wl.E, wl.k
+    R = rows_alloc_for("dynamic", T, k, E, 21, 20)
+    L = MoELayer(T, wl.d, E, k, wl.f, wl.act, torch.bfloat16, R, backward=True)
+    x, w1, w3, w2, wg = (to_dev(a, dt) for a in (I.x, I.w1, I.w3, I.w2, I.w_g))
+    c_dev = torch.from_numpy(np.tile(np.arange(k, dtype=np.int32), (T, 1))).to(dev())
+    unchanged = torch.zeros(1, dtype=torch.int32, device=dev())
+    for gs in (None, torch.cuda.Stream()):
+        with pytest.raises(ValueError):
+            L.forward_cached(x, w1, w3, w2, cached=c_dev, cache_out=c_dev, unchanged=unchanged,
+                             w_g=wg, renorm=wl.renorm, capacity=("dynamic", 21, 20),
+                             gate_stream=gs)
+    torch.cuda.synchronize()
+    assert int(unchanged.item()) == 0
+
+
 # ---- capacity policy at the launch frontier ---------------------------------------
 # the grow / shrink settings of the benchmark's policy sweep, on its two shapes
 # (T, E, k of the largest layer and of the 64-expert top-1 layer)

@@ -148,3 +148,33 @@ def test_gate_weights_raw_renorm_and_soft_mixture():
     wE = O.gate_weights(p, idsE, renorm=1)
     np.testing.assert_allclose(np.take_along_axis(p, idsE.astype(np.int64), 1), wE,
                                rtol=2e-7)
+
+
+@pytest.mark.parametrize("renorm", [0, 1])
+def test_invalid_cached_id_is_no_pick(renorm):
+    """An id outside [0, E) in cached picks is not a pick (weight 0, out of the
+    normalisation): each row's weights and gate gradients equal those of the
+    same row with that column removed, computed with k - 1 picks."""
+    rng = np.random.default_rng(17)
+    T, E, k, d = 40, 6, 3, 5
+    logits = rng.standard_normal((T, E)) * 2
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    bad_j = rng.integers(0, k, T)
+    bad = ids.copy()
+    bad[np.arange(T), bad_j] = np.where(np.arange(T) % 2 == 0, E + 3, -1)
+    dw = rng.standard_normal((T, k))
+    dw[np.arange(T), bad_j] = 0.0                  # a dropped assignment's dweight
+    x = rng.standard_normal((T, d))
+    p = O.softmax(logits)
+    w_bad = O.gate_weights(p, bad, renorm)
+    dl_bad, _ = O.gate_bwd(logits, bad, dw, renorm, x)
+    for t in range(T):
+        keep = [j for j in range(k) if j != bad_j[t]]
+        w_ref = O.gate_weights(p[t:t + 1], ids[t:t + 1, keep], renorm)
+        np.testing.assert_array_equal(w_bad[t, keep], w_ref[0])
+        assert w_bad[t, bad_j[t]] == 0.0
+        dl_ref, _ = O.gate_bwd(logits[t:t + 1], ids[t:t + 1, keep], dw[t:t + 1, keep], renorm,
+                               x[t:t + 1])
+        np.testing.assert_allclose(dl_bad[t], dl_ref[0], rtol=0, atol=1e-15)
+    # the k - 1 computation is itself the full backward: rows sum to 0
+    np.testing.assert_allclose(dl_bad.sum(axis=1), 0.0, atol=1e-6)
