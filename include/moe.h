@@ -157,6 +157,30 @@ moe_status moe_dispatch(void* stream, moe_dtype dt, int T, int d, int E, int k,
                         int32_t* status, void* workspace,
                         size_t workspace_bytes);
 
+/*
+ * moe_dispatch_noalloc - moe_dispatch for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same arguments, results and errors,
+ * without the workspace.  Its scratch (the routing histograms) is a fixed
+ * device array inside the library, 1 MiB + 256 bytes, one copy per GPU,
+ * held until the process ends.  The call allocates nothing.
+ *   T*k must not exceed moe_dispatch_noalloc_max_assignments() (2^21);
+ *   larger requests return MOE_EWORKSPACE and enqueue nothing.
+ *   The stream must belong to the current device (else MOE_EINVAL).
+ * Every call on one GPU uses that GPU's array: calls that overlap on one
+ * GPU (other streams, other host threads) race and must be ordered by the
+ * caller.  Nothing carries over between calls.
+ */
+moe_status moe_dispatch_noalloc(void* stream, moe_dtype dt, int T, int d, int E, int k,
+                                const void* x, const int32_t* ids,
+                                const int32_t* capacity, const int32_t* offsets,
+                                int64_t rows_alloc, int32_t* counts, int32_t* fill,
+                                int32_t* dest_row, int32_t* src, void* x_disp,
+                                int32_t* status);
+
+/* Largest T*k moe_dispatch_noalloc accepts. [host] */
+size_t moe_dispatch_noalloc_max_assignments(void);
+
 /* Workspace bytes of moe_expert_ffn_fwd / moe_expert_ffn_bwd. [host] */
 size_t moe_ffn_fwd_workspace_bytes(moe_dtype dt, moe_act act, int E, int d,
                                    int f, int64_t rows_alloc);

@@ -33,6 +33,9 @@ SIGNATURES = {
     "moe_dispatch_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int]),
     "moe_dispatch": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_int, _p, _p, _p, _p,
                               _c_i64, _p, _p, _p, _p, _p, _p, _p, _c_size]),
+    "moe_dispatch_noalloc": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_int, _p, _p, _p,
+                                      _p, _c_i64, _p, _p, _p, _p, _p, _p]),
+    "moe_dispatch_noalloc_max_assignments": (_c_size, []),
     "moe_ffn_fwd_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_i64]),
     "moe_ffn_bwd_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_i64]),
     "moe_expert_ffn_fwd": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_int, _p, _p,
@@ -201,6 +204,27 @@ def moe_dispatch(x, ids, E, capacity, offsets, rows_alloc, counts, fill, dest_ro
                               _ptr(offsets), rows_alloc, _ptr(counts), _ptr(fill),
                               _ptr(dest_row), _ptr(src), _ptr(x_disp), _ptr(status), _ptr(ws),
                               _nbytes(ws)), "moe_dispatch")
+
+
+def moe_dispatch_noalloc_max_assignments() -> int:
+    return lib().moe_dispatch_noalloc_max_assignments()
+
+
+def moe_dispatch_noalloc(x, ids, E, capacity, offsets, rows_alloc, counts, fill, dest_row, src,
+                         x_disp, status):
+    """moe_dispatch without a workspace (the library's fixed device scratch)."""
+    T, d = x.shape
+    k = ids.shape[1]
+    _need(ids, T * k, "ids", _I32)
+    for t, n, name in ((capacity, E, "capacity"), (offsets, E + 1, "offsets"),
+                       (counts, E, "counts"), (fill, E, "fill"), (dest_row, T * k, "dest_row"),
+                       (src, rows_alloc, "src"), (status, 1, "status")):
+        _need(t, n, name, _I32)
+    _need(x_disp, rows_alloc * d, "x_disp", x.dtype)
+    _check(lib().moe_dispatch_noalloc(_stream(), _dt(x), T, d, E, k, _ptr(x), _ptr(ids),
+                                      _ptr(capacity), _ptr(offsets), rows_alloc, _ptr(counts),
+                                      _ptr(fill), _ptr(dest_row), _ptr(src), _ptr(x_disp),
+                                      _ptr(status)), "moe_dispatch_noalloc")
 
 
 def moe_ffn_fwd_workspace_bytes(dt, act, E, d, f, rows_alloc) -> int:

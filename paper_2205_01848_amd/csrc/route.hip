@@ -13,6 +13,7 @@
 // one wavefront per token, 16-byte vector loads/stores along the row, so x
 // is read once even when k rows are written.
 
+#include <mutex>
 #include <type_traits>
 
 #include "common.hpp"
@@ -557,21 +558,49 @@ extern "C" size_t moe_dispatch_workspace_bytes(int T, int E, int k) {
   return align_up((2 * nblk * E + E) * sizeof(int32_t), 256);
 }
 
-extern "C" moe_status moe_dispatch(void* stream, moe_dtype dt, int T, int d, int E, int k,
-                                   const void* x, const int32_t* ids,
-                                   const int32_t* capacity, const int32_t* offsets,
-                                   int64_t rows_alloc, int32_t* counts, int32_t* fill,
-                                   int32_t* dest_row, int32_t* src, void* x_disp,
-                                   int32_t* status, void* workspace, size_t workspace_bytes) {
+static moe_status dispatch_args_ok(moe_dtype dt, int T, int d, int E, int k, const void* x,
+                                   const int32_t* ids, const int32_t* capacity,
+                                   const int32_t* offsets, int64_t rows_alloc,
+                                   const int32_t* counts, const int32_t* fill,
+                                   const int32_t* dest_row, const int32_t* src,
+                                   const void* x_disp, const int32_t* status) {
   if (!dtype_ok(dt) || !shape_ok(T, E, k) || !width_ok(d) || !rows_ok(rows_alloc))
     return MOE_EINVAL;
   if (!capacity || !offsets || !counts || !fill || !status) return MOE_EINVAL;
   if (rows_alloc > 0 && (!src || !x_disp)) return MOE_EINVAL;
   if (T > 0 && (!x || !ids || !dest_row)) return MOE_EINVAL;
   if ((x && !aligned16(x)) || (x_disp && !aligned16(x_disp))) return MOE_EINVAL;
+  return MOE_OK;
+}
+
+// The launches of moe_dispatch; `workspace` holds moe_dispatch_workspace_bytes.
+static moe_status dispatch_launch(hipStream_t s, moe_dtype dt, int T, int d, int E, int k,
+                                  const void* x, const int32_t* ids, const int32_t* capacity,
+                                  const int32_t* offsets, int64_t rows_alloc, int32_t* counts,
+                                  int32_t* fill, int32_t* dest_row, int32_t* src, void* x_disp,
+                                  int32_t* status, void* workspace);
+
+extern "C" moe_status moe_dispatch(void* stream, moe_dtype dt, int T, int d, int E, int k,
+                                   const void* x, const int32_t* ids,
+                                   const int32_t* capacity, const int32_t* offsets,
+                                   int64_t rows_alloc, int32_t* counts, int32_t* fill,
+                                   int32_t* dest_row, int32_t* src, void* x_disp,
+                                   int32_t* status, void* workspace, size_t workspace_bytes) {
+  const moe_status st = dispatch_args_ok(dt, T, d, E, k, x, ids, capacity, offsets, rows_alloc,
+                                         counts, fill, dest_row, src, x_disp, status);
+  if (st != MOE_OK) return st;
   const size_t need = moe_dispatch_workspace_bytes(T, E, k);
   if (!workspace || workspace_bytes < need) return MOE_EWORKSPACE;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dispatch_launch(static_cast<hipStream_t>(stream), dt, T, d, E, k, x, ids, capacity,
+                         offsets, rows_alloc, counts, fill, dest_row, src, x_disp, status,
+                         workspace);
+}
+
+static moe_status dispatch_launch(hipStream_t s, moe_dtype dt, int T, int d, int E, int k,
+                                  const void* x, const int32_t* ids, const int32_t* capacity,
+                                  const int32_t* offsets, int64_t rows_alloc, int32_t* counts,
+                                  int32_t* fill, int32_t* dest_row, int32_t* src, void* x_disp,
+                                  int32_t* status, void* workspace) {
   const int nblk = route_nblk(T, k);
   int32_t* hist = static_cast<int32_t*>(workspace);
   int32_t* base = hist + static_cast<size_t>(nblk) * E;
@@ -608,6 +637,70 @@ extern "C" moe_status moe_dispatch(void* stream, moe_dtype dt, int T, int d, int
       static_cast<const uint4*>(x), dest_row, T, k, nvec, static_cast<uint4*>(x_disp));
   MOE_LAUNCH_CHECK();
   return MOE_OK;
+}
+
+// ---- allocation-free dispatch ------------------------------------------------
+// moe_dispatch_noalloc keeps the routing histograms in `scratch`, a fixed
+// device array of this library, instead of a caller workspace.  Each GPU
+// holds its own copy at its own address; the host looks that address up once
+// per device and passes it to the kernels (the array's name in host code is
+// only a host-side stand-in).  Every call on one GPU shares the array, so
+// calls that overlap on one GPU race.  Nothing in it needs clearing: the
+// histogram kernel writes every entry the scan and rank kernels read.
+constexpr int64_t kNoAllocMaxAssignments = int64_t(1) << 21;  // T*k limit
+constexpr size_t kNoAllocScratchBytes =
+    (2 * static_cast<size_t>(kNoAllocMaxAssignments / kChunk) * kMaxE + kMaxE) * sizeof(int32_t);
+static_assert(kNoAllocScratchBytes % 256 == 0, "scratch size is whole 256-byte blocks");
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_dev[kMaxDevices];  // device address of `scratch`, per device
+
+// Device address of this device's `scratch` (looked up on the first call
+// made with that device current).
+static moe_status scratch_address(hipStream_t s, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MOE_EHIP;
+  if (s != nullptr) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(s, &sdev) != hipSuccess) return MOE_EHIP;
+    if (sdev != dev) return MOE_EINVAL;  // the stream must belong to the current device
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return MOE_EHIP;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return MOE_OK;
+}
+
+extern "C" size_t moe_dispatch_noalloc_max_assignments(void) {
+  return static_cast<size_t>(kNoAllocMaxAssignments);
+}
+
+extern "C" moe_status moe_dispatch_noalloc(void* stream, moe_dtype dt, int T, int d, int E,
+                                           int k, const void* x, const int32_t* ids,
+                                           const int32_t* capacity, const int32_t* offsets,
+                                           int64_t rows_alloc, int32_t* counts, int32_t* fill,
+                                           int32_t* dest_row, int32_t* src, void* x_disp,
+                                           int32_t* status) {
+  const moe_status st = dispatch_args_ok(dt, T, d, E, k, x, ids, capacity, offsets, rows_alloc,
+                                         counts, fill, dest_row, src, x_disp, status);
+  if (st != MOE_OK) return st;
+  if (static_cast<int64_t>(T) * k > kNoAllocMaxAssignments ||
+      moe_dispatch_workspace_bytes(T, E, k) > kNoAllocScratchBytes)
+    return MOE_EWORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  const moe_status sa = scratch_address(s, &ws);
+  if (sa != MOE_OK) return sa;
+  return dispatch_launch(s, dt, T, d, E, k, x, ids, capacity, offsets, rows_alloc, counts, fill,
+                         dest_row, src, x_disp, status, ws);
 }
 
 extern "C" moe_status moe_combine(void* stream, moe_dtype dt, int T, int d, int k,
