@@ -81,3 +81,16 @@ def min_topk_gap(logits, k):
     for j in range(k - 1):
         gaps = np.minimum(gaps, np.abs(l[:, j] - l[:, j + 1]))
     return float(gaps.min())
+
+
+def relu_kink_bound(n_values, eps=1e-5):
+    """Upper bound on how many of n_values ReLU pre-activations fall within
+    eps * rms of 0 (where fp32 summation order, not the arithmetic, decides
+    relu'(H), so the row is excluded from the dX comparison).  For a
+    pre-activation close to normal with standard deviation sigma = rms,
+    P(|h| < eps sigma) = erf(eps / sqrt 2) ~ 0.80 eps; the mean is doubled
+    for experts whose own scale is below the tensor's rms, then six standard
+    deviations of a Poisson count and a floor of 4 are added."""
+    import math
+    mu = 2 * 0.8 * eps * n_values
+    return int(mu + 6 * math.sqrt(mu) + 4)

@@ -6,8 +6,8 @@ configuration bench.py's variants time:
   all tokens; the gate backward with it on sampled tokens;
 * AggregateSpec and the specification loss (Eq. 2): sampled (token,
   choice) rows against the oracle's expert rows, dweights and dy_disp rows of
-  sampled tokens, and the loss against the sum the kernel's own dweights
-  imply (a property that holds at any size);
+  sampled tokens end to end; the loss, all dweights and all kept dy_disp
+  rows stage-wise (the oracle's Eq. 2 on the kernel's expert rows);
 * caching (Section 4.2): the unchanged-sample count over all tokens, the
   weights at cached picks, and sampled layer outputs with the gate on a
   second stream;
@@ -130,9 +130,21 @@ def test_balance_and_spec_loss_full_size(c5):
     dwg = to_np(L.dweights)
     assert_close(to_np(L.spec_loss_value), np.array([(to_np(L.weights) * dwg).sum()]), 1e-5,
                  "spec loss vs its dweights")
+    # stage-wise over all tokens: the oracle's Eq. 2 on the kernel's expert
+    # rows (checked on the sample above) gives the loss, every dweight and
+    # every kept dy_disp row
+    Yd = to_np(L.y_disp)
+    loss_all, dw_all, dY_all = O.spec_loss(Yd, dest, wts, Tgt, "bf16")
+    del Yd
+    assert_close(to_np(L.spec_loss_value), np.array([loss_all]), 1e-5, "spec loss (all tokens)")
+    assert_close(dwg, dw_all, 1e-4, "spec dweights (all tokens)")
+    kept_rows = s["src"] >= 0
+    assert_close(to_np(L.dy_disp)[:R][kept_rows], dY_all[kept_rows], rt,
+                 "spec dy_disp (all kept rows)")
+    del dY_all
     # gate backward with the balance coefficient, sampled tokens
     dl_ref, _ = O.gate_bwd(logits[toks], ids[toks], dwg[toks], wl.renorm, X[toks],
-                           dprob_coef=to_np(L.dprob_coef))
+                           dprob_coef=coef)
     assert_close(to_np(L.dlogits)[toks], dl_ref, 1e-5, "dlogits with balance term")
 
 

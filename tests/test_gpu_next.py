@@ -179,12 +179,13 @@ def test_layer_backward_with_spec_loss_and_balance(name, lam):
     fw = O.layer_forward(X, W1, W3, W2, wl.act, dt, r["ids"], r["weights"], cap, R, wl.E)
     Bref, coef = O.balance_term(r["logits"], counts, wl.k, lam)
     assert_close(to_np(L.balance_loss), np.array([Bref]), 1e-5, "balance loss")
+    assert_close(to_np(L.dprob_coef), coef, 1e-6, "dprob coefficient")
     rt = RTOL[dt]
     agg = O.aggregate_spec(np.nan_to_num(fw["Y"]), fw["dest_row"])
     assert_close(to_np(spec_rows), agg, rt, "AggregateSpec rows")
     bw = O.layer_backward(fw, X, None, W1, W3, W2, wl.act, dt, r["ids"], r["weights"], wl.E,
                           logits=r["logits"], renorm=wl.renorm, w_g=_dec(I.w_g, dt),
-                          target=_dec(tgt, dt), dprob_coef=to_np(L.dprob_coef))
+                          target=_dec(tgt, dt), dprob_coef=coef)
     assert_close(to_np(L.spec_loss_value), np.array([bw["spec_loss"]]), rt, "spec loss")
     assert_close(to_np(L.dweights), bw["dweights"], rt, "dweights")
     assert_close(to_np(L.dw1), bw["dW1"], rt, "dW1")
