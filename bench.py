@@ -71,6 +71,12 @@ def parse():
                          "of mini-batches, drops vs average capacity factor for static "
                          "capacities and for launch-frontier policies")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--configs", action="store_true",
+                    help="also time every other workload into detail.configs (the default "
+                         "c5 run does this unless --no-configs)")
+    ap.add_argument("--no-configs", action="store_true")
+    ap.add_argument("--reps", type=int, default=50,
+                    help="repetitions per run of detail.configs (median reported)")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time its replays (per-kernel "
                          "times then come from as many instrumented eager steps)")
@@ -111,8 +117,9 @@ def gemm_flops(wl, kept):
     return fl
 
 
-def hbm_bytes(wl, kept, active):
-    """Algorithmic HBM bytes per launch of the row-moving kernels."""
+def hbm_bytes(wl, kept, active, padded=0):
+    """Algorithmic HBM bytes per launch of the row-moving kernels (`padded`:
+    rows the padded static baseline zeroes beyond the kept ones)."""
     s, T, d, E, k = wl.esize, wl.T, wl.d, wl.E, wl.k
     b = {
         "gate_fwd": T * d * s + E * d * s + T * E * 4 + T * k * 8,
@@ -131,6 +138,8 @@ def hbm_bytes(wl, kept, active):
     b["spec_loss"] = 2 * kept * d * s + T * d * s + T * k * 12
     b["cache_update"] = 3 * T * k * 4
     b["cached_weights"] = T * E * 4 + 2 * T * k * 4
+    if padded:
+        b["zero_pad_rows"] = padded * d * s
     return b
 
 
@@ -182,7 +191,8 @@ def cpu_baseline(wl, I, cap_rule, ntok):
                          logits=logits, renorm=wl.renorm, w_g=WG)
     el = time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()] + [1])
-    return {"value": ntok / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    return {"value": ntok / el, "unit": "tokens/s", "cores": int(threads),
+            "host_cpus": os.cpu_count(), "kind": "oracle",
             "sample": f"first {ntok} of {wl.T} tokens of the workload, "
                       f"{'forward+backward' if wl.backward else 'forward'}, float64 numpy "
                       f"({el:.1f} s)"}
@@ -286,37 +296,15 @@ def policy_sweep(args):
     print(json.dumps(out))
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer is not "
-              "sharded across GPUs.", file=sys.stderr)
-        sys.exit(2)
-    if args.copy_gib > 0:
-        copy_calibration(args.copy_gib, args.steps)
-        return
-    if args.policy_sweep:
-        policy_sweep(args)
-        return
+def upload(wl, dev):
+    """Seeded inputs of a workload, resident in device memory."""
     import numpy as np
     import torch
 
     import workloads as W
-    from paper_2205_01848_amd import MoELayer, binding as B, rows_alloc_for
-
-    wl = W.config(args.workload)
-    cap_rule = wl.capacity[-1]
-    if args.capacity:
-        kind, frac = args.capacity.split(":")
-        num, den = (int(v) for v in frac.split("/"))
-        cap_rule = (kind, num, den)
-    dev = torch.device("cuda:0")
-    log(f"workload {args.workload}: generating inputs")
-    t_gen = time.perf_counter()
+    t0 = time.perf_counter()
     I = W.make_inputs(wl)
-    t_gen = time.perf_counter() - t_gen
-    log(f"inputs ready in {t_gen:.1f} s; uploading")
-    td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    t_gen = time.perf_counter() - t0
 
     def up(a):
         if a is None:
@@ -324,7 +312,16 @@ def main():
         if wl.dtype == "bf16" and a.dtype == np.uint16:
             return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
         return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    return I, up, t_gen
 
+
+def build_step(wl, I, up, cap_rule, rows, variant, args, dev):
+    """The layer, its device inputs and one step (closure) for this run."""
+    import torch
+
+    import workloads as W
+    from paper_2205_01848_amd import MoELayer, binding as B, rows_alloc_for
+    td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     x, w1, w3, w2, dy = (up(a) for a in (I.x, I.w1, I.w3, I.w2, I.dy))
     kind, num, den = cap_rule
     R = rows_alloc_for(kind, wl.T, wl.k, wl.E, num, den)
@@ -337,7 +334,6 @@ def main():
         fkw = dict(ids=up(I.ids), weights=up(I.cw))
         bkw = dict(weights=fkw["weights"])
 
-    variant = args.variant
     if variant in ("balance", "cached") and wl.gate != "linear":
         raise SystemExit(f"--variant {variant} needs a workload with a gate")
     if variant in ("balance", "spec", "cached") and not wl.backward:
@@ -359,30 +355,160 @@ def main():
         init = [-(-T_ * k_ // E_)] * E_                 # Eq. 4 with alpha = 1
         grow = (cap_rule[1], cap_rule[2]) if cap_rule[0] == "dynamic" else (21, 20)
         extra["policy"] = B.CapacityPolicy(T_, k_, E_, args.delta, grow, (5, 4), init)
-        extra["recompiles"] = 0
 
     def step():
         if variant == "cached":
             L.forward_cached(x, w1, w3, w2, cached=extra["cached"], cache_out=extra["cache_out"],
                              unchanged=extra["unchanged"], w_g=fkw["w_g"], bias=fkw["bias"],
                              renorm=wl.renorm, capacity=cap_rule, gate_stream=extra["gate_stream"],
-                             rows=args.rows)
-            L.backward(x, dy, w1, w3, w2, rows=args.rows, ids=extra["cached"],
+                             rows=rows)
+            L.backward(x, dy, w1, w3, w2, rows=rows, ids=extra["cached"],
                        weights=L.cached_weights, **bkw)
             return
         if variant == "policy":
             rows_needed, _ = extra["policy"].begin(L.capacity, L.offsets)
             if rows_needed > L.rows_alloc:
                 raise SystemExit(f"policy asks for {rows_needed} rows > {L.rows_alloc}")
-            L.forward(x, w1, w3, w2, capacity=("policy", 1, 1), rows=args.rows, **fkw)
+            L.forward(x, w1, w3, w2, capacity=("policy", 1, 1), rows=rows, **fkw)
             extra["policy"].end(L.counts)
         else:
-            L.forward(x, w1, w3, w2, capacity=cap_rule, rows=args.rows,
+            L.forward(x, w1, w3, w2, capacity=cap_rule, rows=rows,
                       balance=args.lam if variant == "balance" else None, **fkw)
         if variant == "spec":
             L.aggregate_spec(extra["spec_rows"])
         if wl.backward:
-            L.backward(x, dy, w1, w3, w2, rows=args.rows, target=extra.get("target"), **bkw)
+            L.backward(x, dy, w1, w3, w2, rows=rows, target=extra.get("target"), **bkw)
+
+    return L, step, extra
+
+
+def kernel_table(wl, kern, kern_ms, kept, executed, active):
+    """Per-kernel rates from the library's timing report, the dominant kernel
+    and the GEMM totals."""
+    fl_alg = gemm_flops(wl, kept)
+    by = hbm_bytes(wl, kept, active, executed - kept)
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    detail = {}
+    for name, (n, ms) in kern.items():
+        avg = ms / max(n, 1)
+        row = {"launches": n, "avg_ms": round(avg, 4), "share": round(ms / kern_ms, 4)}
+        if name in fl_alg:
+            row["tflops"] = round(fl_alg[name] / avg / 1e9, 1)
+            row["frac_mfma_peak"] = round(fl_alg[name] / avg / 1e9 / peak, 4)
+        if name in by:
+            row["gbs"] = round(by[name] / avg / 1e6, 1)
+            row["frac_hbm"] = round(by[name] / avg / 1e6 / PEAK_HBM_GBS, 4)
+        detail[name] = row
+    dom = max(kern.items(), key=lambda kv: kv[1][1])[0] if kern else None
+    gemm_ms = sum(kern[k][1] for k in kern if k in fl_alg)
+    gemm_fl = sum(fl_alg[k] * kern[k][0] for k in kern if k in fl_alg)
+    gemm = round(gemm_fl / (gemm_ms / 1e3) / 1e12, 1) if gemm_ms else None
+    return detail, dom, gemm, round(gemm_ms / kern_ms, 4), fl_alg, by, peak
+
+
+# extra runs reported in detail.configs of the default run: every workload,
+# with the static-capacity runs both on kept rows and padded to capacity
+EXTRA_RUNS = [("c1", 0, "fill"), ("c2", 1, "fill"), ("c2", 0, "fill"), ("c2", 0, "capacity"),
+              ("c3", 1, "fill"), ("c3", 0, "fill"), ("c3", 0, "capacity"), ("c4", 0, "fill")]
+FLUSH_BYTES = 512 << 20       # scratch written between repetitions (> the 256 MB MALL)
+
+
+def median_runs(args, dev):
+    """detail.configs: each run's median step over args.reps repetitions
+    (uninstrumented, a FLUSH_BYTES scratch write before each, so no
+    repetition finds the last one's data in the L2 or the MALL), then the
+    same number of instrumented repetitions (flushed the same way) for the
+    per-kernel rates."""
+    import statistics
+
+    import torch
+
+    import workloads as W
+    from paper_2205_01848_amd import binding as B
+    scratch = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    out = []
+    cache = {}
+    for name, run, rows in EXTRA_RUNS:
+        wl = W.config(name)
+        cap_rule = wl.capacity[run]
+        if name not in cache:
+            cache.clear()
+            torch.cuda.empty_cache()
+            cache[name] = upload(wl, dev)
+        I, up, _ = cache[name]
+        log(f"config {name} capacity {cap_rule} rows={rows}: {args.reps} reps")
+        L, step, _ = build_step(wl, I, up, cap_rule, rows, "base", args, dev)
+        for _ in range(max(args.warmup, 2)):
+            step()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.reps)]
+        for i in range(args.reps):
+            scratch.fill_(i & 0xFF)
+            ev[i][0].record()
+            step()
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        times = [a.elapsed_time(b) for a, b in ev]
+        med = statistics.median(times)
+        B.moe_timing_report()
+        B.moe_timing_enable(True)
+        for i in range(args.reps):
+            scratch.fill_((i + 128) & 0xFF)
+            step()
+        torch.cuda.synchronize()
+        B.moe_timing_enable(False)
+        kern = B.moe_timing_report()
+        kern_ms = sum(ms for _, ms in kern.values())
+        kept = int(L.fill.sum().item())
+        executed = int((L.fill if rows == "fill" else L.capacity).sum().item())
+        active = int((L.dest_row >= 0).any(dim=1).sum().item())
+        detail, dom, gemm, gshare, _, _, _ = kernel_table(wl, kern, kern_ms, kept, executed, active)
+        out.append({"workload": f"{name}: {DESCR[name]}".split(",")[0],
+                    "capacity": f"{cap_rule[0]} {cap_rule[1]}/{cap_rule[2]}", "rows": rows,
+                    "pass": "fwd+bwd" if wl.backward else "fwd",
+                    "ms_per_step_median": round(med, 4),
+                    "ms_per_step_min": round(min(times), 4),
+                    "tokens_per_s": round(wl.T / (med / 1e3), 1), "reps": args.reps,
+                    "flush_bytes": FLUSH_BYTES, "kept_rows": kept, "executed_rows": executed,
+                    "status": int(L.status.item()), "gemm_tflops": gemm, "gemm_share": gshare,
+                    "dominant": dom, "kernels": detail})
+        del L, step
+    del scratch
+    cache.clear()
+    torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer is not "
+              "sharded across GPUs.", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_gib > 0:
+        copy_calibration(args.copy_gib, args.steps)
+        return
+    if args.policy_sweep:
+        policy_sweep(args)
+        return
+    import torch
+
+    import workloads as W
+    from paper_2205_01848_amd import binding as B
+
+    wl = W.config(args.workload)
+    cap_rule = wl.capacity[-1]
+    if args.capacity:
+        kind, frac = args.capacity.split(":")
+        num, den = (int(v) for v in frac.split("/"))
+        cap_rule = (kind, num, den)
+    dev = torch.device("cuda:0")
+    log(f"workload {args.workload}: generating inputs")
+    I, up, t_gen = upload(wl, dev)
+    log(f"inputs ready in {t_gen:.1f} s")
+    variant = args.variant
+    L, step, extra = build_step(wl, I, up, cap_rule, args.rows, variant, args, dev)
 
     warmup = args.warmup
     if variant == "policy":
@@ -435,28 +561,12 @@ def main():
     kern = B.moe_timing_report()
     ms_step = total_ms / args.steps
 
-    # per-kernel rates
-    fl = gemm_flops(wl, executed)
-    fl_alg = gemm_flops(wl, kept)
-    by = hbm_bytes(wl, kept, active)
-    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
-    detail = {}
-    for name, (n, ms) in kern.items():
-        avg = ms / max(n, 1)
-        row = {"launches": n, "avg_ms": round(avg, 4), "share": round(ms / kern_ms, 4)}
-        if name in fl:
-            row["tflops"] = round(fl_alg[name] / avg / 1e9, 1)
-            row["frac_mfma_peak"] = round(fl_alg[name] / avg / 1e9 / peak, 4)
-        if name in by:
-            row["gbs"] = round(by[name] / avg / 1e6, 1)
-            row["frac_hbm"] = round(by[name] / avg / 1e6 / PEAK_HBM_GBS, 4)
-        detail[name] = row
-    dom = max(kern.items(), key=lambda kv: kv[1][1])[0] if kern else None
+    detail, dom, gemm, gshare, fl_alg, by, peak = kernel_table(wl, kern, kern_ms, kept, executed,
+                                                              active)
     roof = None
-    if dom in fl:
+    if dom in fl_alg:
         n, ms = kern[dom]
-        avg_s = ms / n / 1e3
-        ach = fl_alg[dom] / avg_s / 1e12
+        ach = fl_alg[dom] / (ms / n / 1e3) / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1), "peak": peak,
                 "unit": "TFLOP/s", "frac": round(ach / peak, 4),
                 "traffic": profiled_traffic(args.workload, dom)}
@@ -466,13 +576,6 @@ def main():
         roof = {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
                 "traffic": profiled_traffic(args.workload, dom)}
-    gemm_ms = sum(kern[k][1] for k in kern if k in fl)
-    gemm_fl = sum(fl_alg[k] * kern[k][0] for k in kern if k in fl)
-
-    log(f"{ms_step:.3f} ms/step; oracle baseline")
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, I, cap_rule, CPU_SAMPLE[args.workload])
 
     out = {
         "metric": METRIC,
@@ -495,10 +598,9 @@ def main():
                    "rows": args.rows, "pass": "fwd+bwd" if wl.backward else "fwd",
                    "parallelism": "single GPU"},
         "roofline": roof,
-        "cpu_baseline": cpu,
+        "cpu_baseline": None,
         "detail": {"kept_rows": kept, "executed_rows": executed, "status": status,
-                   "gemm_tflops": round(gemm_fl / (gemm_ms / 1e3) / 1e12, 1) if gemm_ms else None,
-                   "gemm_share": round(gemm_ms / kern_ms, 4),
+                   "gemm_tflops": gemm, "gemm_share": gshare,
                    "input_gen_s": round(t_gen, 1), "kernels": detail},
     }
     if graph is not None:
@@ -522,6 +624,17 @@ def main():
                                    "capacity": st["cap"],
                                    "capacity_factor": round(sum(st["cap"]) / (wl.T * wl.k), 4)}
         extra["policy"].close()
+    log(f"{ms_step:.3f} ms/step")
+    del L, step, extra
+    torch.cuda.empty_cache()
+
+    headline_default = (args.workload == "c5" and variant == "base" and args.rows == "fill"
+                        and not args.capacity and not args.graph)
+    if args.configs or (headline_default and not args.no_configs):
+        out["detail"]["configs"] = median_runs(args, dev)
+    if not args.no_cpu_baseline:
+        log("oracle baseline")
+        out["cpu_baseline"] = cpu_baseline(wl, I, cap_rule, CPU_SAMPLE[args.workload])
     print(json.dumps(out))
 
 
