@@ -80,6 +80,10 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time its replays (per-kernel "
                          "times then come from as many instrumented eager steps)")
+    ap.add_argument("--blas-gemm", default=None, metavar="M,N,K",
+                    help="instead of the layer: time hipBLASLt (torch.matmul) on one bf16 "
+                         "product C[M,N] = A[M,K] B[N,K]^T with N(0,1) operands (context: "
+                         "an achievable GEMM rate on this GPU; not part of the path)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead of the layer: time a plain device-to-device copy of this "
                          "many GiB (achievable HBM bandwidth; byte-counter calibration)")
@@ -103,6 +107,31 @@ def copy_calibration(gib, steps):
     ms = e0.elapsed_time(e1) / steps
     print(json.dumps({"copy_bytes_each_way": n, "ms_per_copy": round(ms, 4),
                       "hbm_GBps_read_plus_write": round(2 * n / (ms / 1e3) / 1e9, 1)}))
+
+
+def blas_gemm(shape, steps, warmup):
+    """hipBLASLt through torch.matmul on A [M,K] times B [N,K]^T (both operands
+    K-contiguous, as every forward product of the layer reads them)."""
+    import torch
+    M, N, K = (int(v) for v in shape.split(","))
+    g = torch.Generator(device="cuda:0").manual_seed(1)
+    a = torch.randn(M, K, device="cuda:0", dtype=torch.bfloat16, generator=g)
+    b = torch.randn(N, K, device="cuda:0", dtype=torch.bfloat16, generator=g)
+    c = torch.empty(M, N, device="cuda:0", dtype=torch.bfloat16)
+    for _ in range(warmup):
+        torch.matmul(a, b.t(), out=c)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        torch.matmul(a, b.t(), out=c)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(json.dumps({"blas_gemm": [M, N, K], "ms": round(ms, 4),
+                      "tflops": round(2.0 * M * N * K / (ms / 1e3) / 1e12, 1),
+                      "frac_bf16_peak": round(2.0 * M * N * K / (ms / 1e3) / 1e12 /
+                                              PEAK_BF16_TFLOPS, 4)}))
 
 
 def gemm_flops(wl, kept):
@@ -488,6 +517,9 @@ def main():
         sys.exit(2)
     if args.copy_gib > 0:
         copy_calibration(args.copy_gib, args.steps)
+        return
+    if args.blas_gemm:
+        blas_gemm(args.blas_gemm, args.steps, args.warmup)
         return
     if args.policy_sweep:
         policy_sweep(args)

@@ -51,6 +51,9 @@ def short_name(name: str) -> str:
     if m:
         targs = (m.group(2) or "").replace("unsigned short", "bf16").replace("float", "f32")
         return m.group(1) + targs.replace(" ", "")
+    if "Cijk_" in name:
+        m = re.search(r"MT\d+x\d+x\d+_MI\d+x\d+x\d+", name)
+        return "hipblaslt " + (m.group(0) if m else name[:40])
     return re.sub(r"\(.*", "", name)[:60]
 
 
@@ -74,10 +77,115 @@ def copy_factor(path, counter, nbytes):
     return nbytes / (kib * 1024.0), kib
 
 
+def counter_table(paths):
+    """{short kernel name: {counter: mean value per dispatch, "_ns": mean
+    duration}} over one or more counter-collection CSVs."""
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    durs = collections.defaultdict(dict)
+    for path in paths:
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                n = short_name(r["Kernel_Name"])
+                vals[n][r["Counter_Name"]].append(float(r["Counter_Value"]))
+                key = (path, r["Dispatch_Id"])
+                durs[n][key] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    out = {}
+    for n, cs in vals.items():
+        row = {c: sum(v) / len(v) for c, v in cs.items()}
+        row["_ns"] = sum(durs[n].values()) / len(durs[n])
+        row["_dispatches"] = len(durs[n])
+        out[n] = row
+    return out
+
+
+def derived(row, n_xcd=8, n_simd=1024, n_cu=256):
+    """Per-dispatch figures from the raw counters (values are sums over all
+    instances of a counter; GRBM counters count once per XCD)."""
+    d = {}
+    gui = row.get("GRBM_GUI_ACTIVE")
+    if gui:
+        cyc = gui / n_xcd
+        d["clock_GHz"] = cyc / row["_ns"]
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in row:
+            d["mfma_busy"] = row["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * n_simd)
+        if "SQ_LDS_BANK_CONFLICT" in row:
+            d["lds_conflict_of_cycles"] = row["SQ_LDS_BANK_CONFLICT"] / (cyc * n_cu)
+    if row.get("SQ_WAVE_CYCLES") and "SQ_WAIT_INST_ANY" in row:
+        d["wait_any_of_wave_cycles"] = row["SQ_WAIT_INST_ANY"] / row["SQ_WAVE_CYCLES"]
+    if row.get("SQ_LDS_IDX_ACTIVE") and "SQ_LDS_BANK_CONFLICT" in row:
+        d["lds_conflict_per_access"] = row["SQ_LDS_BANK_CONFLICT"] / max(
+            row["SQ_LDS_IDX_ACTIVE"] - row["SQ_LDS_BANK_CONFLICT"], 1.0)
+    hit, miss = row.get("TCC_HIT_sum"), row.get("TCC_MISS_sum")
+    if hit is not None and miss is not None and hit + miss > 0:
+        d["l2_hit_rate"] = hit / (hit + miss)
+    if "TCC_EA0_RDREQ_sum" in row:
+        d["ea_read_req"] = row["TCC_EA0_RDREQ_sum"]
+    if row.get("TCP_TCC_READ_REQ_sum"):
+        d["l2_read_latency_cycles"] = row["TCP_TCC_READ_REQ_LATENCY_sum"] / row["TCP_TCC_READ_REQ_sum"]
+    return d
+
+
+COUNTER_COLS = [("ms", "ms"), ("clock_GHz", "clock GHz"), ("mfma_busy", "MFMA busy"),
+                ("wait_any_of_wave_cycles", "s_waitcnt share of wave cycles"),
+                ("lds_conflict_of_cycles", "LDS bank-conflict cycles / CU cycles"),
+                ("lds_conflict_per_access", "LDS conflicts per access"),
+                ("l2_hit_rate", "L2 hit rate"), ("ea_read_req", "EA read requests (M)"),
+                ("l2_read_latency_cycles", "L2 read latency (cycles)")]
+
+
+def counters_main(a):
+    tab = counter_table(a.pmc)
+    lines = [f"# rocprofv3 counters: {a.workload}", "",
+             "Commands (run from /tmp with TMPDIR=/tmp; R = repository root):", ""]
+    lines += [f"    {c}" for c in a.command]
+    lines += ["", "Each --pmc group ran in a process of its own; values are means per "
+              "dispatch, sums over every instance of a counter (GRBM counters once per XCD, "
+              "so cycles per XCD = GRBM_GUI_ACTIVE / 8).  clock = GRBM_GUI_ACTIVE / 8 / "
+              "duration; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (cycles x 1024 SIMDs); "
+              "s_waitcnt share = SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES; L2 hit rate = "
+              "TCC_HIT / (TCC_HIT + TCC_MISS); L2 read latency = TCP_TCC_READ_REQ_LATENCY "
+              "/ TCP_TCC_READ_REQ.", "",
+              "| kernel | " + " | ".join(h for _, h in COUNTER_COLS) + " |",
+              "|---" * (len(COUNTER_COLS) + 1) + "|"]
+    keep = [n for n in tab if a.match is None or re.search(a.match, n)]
+    keep.sort(key=lambda n: -tab[n]["_ns"])
+    out = {"workload": a.workload, "source_hash": source_hash(), "kernels": {}}
+    for n in keep[:a.top]:
+        row = tab[n]
+        d = derived(row)
+        d["ms"] = row["_ns"] / 1e6
+        out["kernels"][n] = {"raw": {k: v for k, v in row.items() if not k.startswith("_")},
+                             "derived": d, "dispatches": row["_dispatches"]}
+        cells = []
+        for key, _ in COUNTER_COLS:
+            v = d.get(key)
+            if v is None:
+                cells.append("")
+            elif key == "ea_read_req":
+                cells.append(f"{v / 1e6:.1f}")
+            elif key in ("ms",):
+                cells.append(f"{v:.3f}")
+            elif key == "l2_read_latency_cycles":
+                cells.append(f"{v:.0f}")
+            else:
+                cells.append(f"{v:.3f}")
+        lines.append(f"| {n[:60]} | " + " | ".join(cells) + " |")
+    lines += ["", f"Kernel sources hash: {out['source_hash']}", ""]
+    with open(a.out, "w") as f:
+        f.write("\n".join(lines))
+    if a.json:
+        with open(a.json, "w") as f:
+            json.dump(out, f, indent=1)
+
+
 def main():
     ap = argparse.ArgumentParser()
+    ap.add_argument("--pmc", action="append", default=None,
+                    help="counters mode: counter-collection CSVs (one per --pmc group)")
+    ap.add_argument("--match", default=None, help="counters mode: kernel-name regex")
+    ap.add_argument("--top", type=int, default=16)
     ap.add_argument("--workload", required=True)
-    ap.add_argument("--stats", required=True)
+    ap.add_argument("--stats")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
     ap.add_argument("--copy-fetch")
@@ -87,6 +195,11 @@ def main():
     ap.add_argument("--out", required=True)
     ap.add_argument("--json")
     a = ap.parse_args()
+    if a.pmc:
+        counters_main(a)
+        return
+    if not a.stats:
+        ap.error("--stats is required without --pmc")
 
     rows = []
     with open(a.stats) as f:
