@@ -386,7 +386,42 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
   }
 }
 
-// dx[t] = sum_j kept dx_disp[r_j] (+ dl[t] . w_g).  A wavefront takes a group
+// dx[t] = sum_j kept dx_disp[r_j] on the cached path (no gate term): one
+// wavefront per token streams its whole rows, as the combine does (summed in
+// float32 in order j, one rounding).
+template <typename T>
+__global__ __launch_bounds__(256) void row_sum_kernel(
+    const uint4* __restrict__ dxd, const int32_t* __restrict__ dest_row, int Ttok, int k,
+    int nvec, int64_t rows_alloc, uint4* __restrict__ dx) {
+  constexpr int V = Elem<T>::kVec;
+  const int t = blockIdx.x * kRowWaves + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= Ttok) return;
+  int dst[kMaxK];
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    dst[j] = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
+    if (dst[j] >= rows_alloc) dst[j] = -1;
+  }
+  uint4* o = dx + static_cast<size_t>(t) * nvec;
+  for (int v = lane; v < nvec; v += 64) {
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+      if (dst[j] >= 0) {
+        float f[V];
+        Elem<T>::load(dxd[static_cast<size_t>(dst[j]) * nvec + v], f);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] += f[i];
+      }
+    }
+    o[v] = Elem<T>::store(acc);
+  }
+}
+
+// dx[t] = sum_j kept dx_disp[r_j] + dl[t] . w_g.  A wavefront takes a group
 // of TG tokens (k <= KT) and one 64-vector column chunk of their rows
 // (blockIdx.y), so each w_g vector is loaded once per group rather than once
 // per token, and issues all of the group's row gathers at once.
@@ -394,7 +429,7 @@ template <int KT> struct DispatchBwdShape {
   static constexpr int TG = KT <= 2 ? 8 : 16 / KT;   // tokens per wavefront
 };
 
-template <typename T, bool GATE, int KT>
+template <typename T, int KT>
 __global__ __launch_bounds__(256) void dispatch_bwd_kernel(
     const uint4* __restrict__ dxd, const int32_t* __restrict__ dest_row,
     const float* __restrict__ dl, const uint4* __restrict__ wg, int Ttok, int E, int k,
@@ -441,7 +476,7 @@ __global__ __launch_bounds__(256) void dispatch_bwd_kernel(
           for (int i = 0; i < V; ++i) acc[u][i] += f[i];
         }
     }
-    if constexpr (GATE) {
+    {
       // four w_g vectors in flight per step
       constexpr int kEu = 4;
       for (int e0 = 0; e0 < E; e0 += kEu) {
@@ -766,20 +801,23 @@ extern "C" moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d,
   const uint4* g = static_cast<const uint4*>(w_g);
   uint4* o = static_cast<uint4*>(dx);
   MOE_TIMED("dispatch_bwd", s);
+  if (!dlogits) {
+    if (dt == MOE_BF16)
+      row_sum_kernel<uint16_t><<<nblocks(T, kRowWaves), 256, 0, s>>>(a, dest_row, T, k, nvec,
+                                                                    rows_alloc, o);
+    else
+      row_sum_kernel<float><<<nblocks(T, kRowWaves), 256, 0, s>>>(a, dest_row, T, k, nvec,
+                                                                 rows_alloc, o);
+    MOE_LAUNCH_CHECK();
+    return MOE_OK;
+  }
   auto go = [&](auto kt_tag) {
     constexpr int KT = decltype(kt_tag)::value;
     const dim3 grid(nblocks(T, kRowWaves * DispatchBwdShape<KT>::TG), nblocks(nvec, 64));
-    if (dt == MOE_BF16) {
-      if (dlogits)
-        dispatch_bwd_kernel<uint16_t, true, KT><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
-      else
-        dispatch_bwd_kernel<uint16_t, false, KT><<<grid, 256, 0, s>>>(a, dest_row, nullptr, nullptr, T, E, k, nvec, rows_alloc, o);
-    } else {
-      if (dlogits)
-        dispatch_bwd_kernel<float, true, KT><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
-      else
-        dispatch_bwd_kernel<float, false, KT><<<grid, 256, 0, s>>>(a, dest_row, nullptr, nullptr, T, E, k, nvec, rows_alloc, o);
-    }
+    if (dt == MOE_BF16)
+      dispatch_bwd_kernel<uint16_t, KT><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
+    else
+      dispatch_bwd_kernel<float, KT><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
   };
   if (k <= 1) go(std::integral_constant<int, 1>{});
   else if (k <= 2) go(std::integral_constant<int, 2>{});

@@ -257,15 +257,16 @@ class MoELayer:
     def backward(self, x, dy, w1, w3, w2, *, w_g=None, renorm=0, ids=None, weights=None,
                  rows="fill", target=None):
         """combine_bwd (or, given target, the Eq. 2 specification loss in its
-        place) -> FFN backward -> gate backward -> dispatch backward."""
+        place) -> gate backward -> FFN backward -> dispatch backward.  The
+        gate backward needs only dweights, so it runs before the FFN
+        backward, whose last product (dx_disp) the dispatch backward then
+        reads straight after it was written."""
         if target is not None:
             self.spec_loss(target, self.weights if weights is None else weights)
         else:
             self.combine_bwd(dy, self.weights if weights is None else weights)
-        self.ffn_bwd(w1, w3, w2, rows=rows)
         if w_g is not None:
             self.gate_bwd(x, renorm, ids)
-            self.dispatch_bwd(w_g)
-        else:
-            self.dispatch_bwd(None)
+        self.ffn_bwd(w1, w3, w2, rows=rows)
+        self.dispatch_bwd(w_g)
         return self.dx
