@@ -610,6 +610,57 @@ __device__ __forceinline__ void decode_grouped(int L, int n_mt, int n_nt, int& m
   }
 }
 
+// bf16 tile order, two levels above each XCD's kGroupM x 8 block of tiles.
+// Tiles come in bands of kBandM M-tiles; inside a band, in N-blocks of 8
+// columns, and inside an N-block, in M-blocks of kGroupM rows whose tiles
+// run M fastest.  The blocks of one N-block follow each other, so the 8
+// blocks in flight at once (one per XCD) are 2 N-blocks x 4 M-blocks: 16 x
+// 16 tiles that read 16 + 16 operand panels, against 4 + 64 when the XCDs
+// take 8 N-blocks of the same 4 M-tiles, and a band's A panels stay in the
+// last-level cache while its weight panels stream past.  Partial bands and
+// blocks at the edges keep the same order with fewer rows or columns.
+constexpr int kBandM = 4 * kGroupM;
+__device__ __forceinline__ void decode_banded(int L, int n_mt, int n_nt, int& mt, int& nt) {
+  const int full_bands = n_mt / kBandM;
+  int r, m0, bh;
+  if (L < full_bands * kBandM * n_nt) {
+    const int band = L / (kBandM * n_nt);
+    r = L - band * kBandM * n_nt;
+    m0 = band * kBandM;
+    bh = kBandM;
+  } else {
+    r = L - full_bands * kBandM * n_nt;
+    m0 = full_bands * kBandM;
+    bh = n_mt - m0;
+  }
+  const int full_nb = n_nt / 8;
+  int n0, w;
+  if (r < full_nb * 8 * bh) {
+    const int nb = r / (8 * bh);
+    r -= nb * 8 * bh;
+    n0 = nb * 8;
+    w = 8;
+  } else {
+    r -= full_nb * 8 * bh;
+    n0 = full_nb * 8;
+    w = n_nt - n0;
+  }
+  const int full_mb = bh / kGroupM;
+  int h;
+  if (r < full_mb * kGroupM * w) {
+    const int mb = r / (kGroupM * w);
+    r -= mb * kGroupM * w;
+    m0 += mb * kGroupM;
+    h = kGroupM;
+  } else {
+    r -= full_mb * kGroupM * w;
+    m0 += full_mb * kGroupM;
+    h = bh - full_mb * kGroupM;
+  }
+  mt = m0 + r % h;
+  nt = n0 + r / h;
+}
+
 // The products: PASS names the instance (so each is its own kernel in
 // traces) and fixes the operand layouts.
 enum Pass { P_FWD_H = 0, P_FWD_Y = 1, P_BWD_DA = 2, P_BWD_DX = 3, P_BWD_DW2 = 4, P_BWD_DW13 = 5 };
@@ -1149,7 +1200,7 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
     int slot = -1, mt, nt;
     if constexpr (!VARK) {
       int mti;
-      decode_grouped(L, sc.n_mtiles, p.ntiles, mti, nt);
+      decode_banded(L, sc.n_mtiles, p.ntiles, mti, nt);
       const int2 tm = p.mtile[mti];
       g = tm.x;
       row0 = p.offsets[g] + tm.y;
@@ -1175,7 +1226,7 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
     } else {
       const int tmn = p.mtiles_out * p.ntiles;
       const int si = L / tmn;
-      decode_grouped(L - si * tmn, p.mtiles_out, p.ntiles, mt, nt);
+      decode_banded(L - si * tmn, p.mtiles_out, p.ntiles, mt, nt);
       const int4 sg = p.seg[si];
       g = sg.x;
       slot = sg.w;
