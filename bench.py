@@ -77,6 +77,9 @@ def parse():
     ap.add_argument("--no-configs", action="store_true")
     ap.add_argument("--reps", type=int, default=50,
                     help="repetitions per run of detail.configs (median reported)")
+    ap.add_argument("--row-align", type=int, default=None,
+                    help="rows each expert region of the grouped buffers is aligned to "
+                         "(default: the layer's, one GEMM tile of 256 rows; 1 packs them)")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time its replays (per-kernel "
                          "times then come from as many instrumented eager steps)")
@@ -352,10 +355,12 @@ def build_step(wl, I, up, cap_rule, rows, variant, args, dev):
     from paper_2205_01848_amd import MoELayer, binding as B, rows_alloc_for
     td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     x, w1, w3, w2, dy = (up(a) for a in (I.x, I.w1, I.w3, I.w2, I.dy))
+    from paper_2205_01848_amd.layer import ROW_ALIGN
+    align = ROW_ALIGN if getattr(args, "row_align", None) is None else args.row_align
     kind, num, den = cap_rule
-    R = rows_alloc_for(kind, wl.T, wl.k, wl.E, num, den)
+    R = rows_alloc_for(kind, wl.T, wl.k, wl.E, num, den, align)
     L = MoELayer(wl.T, wl.d, wl.E, wl.k, wl.f, wl.act, td, R, backward=wl.backward,
-                 gate=wl.gate == "linear")
+                 gate=wl.gate == "linear", row_align=align)
     if wl.gate == "linear":
         fkw = dict(w_g=up(I.w_g), bias=None if I.bias is None else up(I.bias), renorm=wl.renorm)
         bkw = dict(w_g=fkw["w_g"], renorm=wl.renorm)
@@ -383,7 +388,8 @@ def build_step(wl, I, up, cap_rule, rows, variant, args, dev):
         T_, k_, E_ = wl.T, wl.k, wl.E
         init = [-(-T_ * k_ // E_)] * E_                 # Eq. 4 with alpha = 1
         grow = (cap_rule[1], cap_rule[2]) if cap_rule[0] == "dynamic" else (21, 20)
-        extra["policy"] = B.CapacityPolicy(T_, k_, E_, args.delta, grow, (5, 4), init)
+        extra["policy"] = B.CapacityPolicy(T_, k_, E_, args.delta, grow, (5, 4), init,
+                                           row_align=L.row_align)
 
     def step():
         if variant == "cached":
@@ -628,7 +634,7 @@ def main():
                    "E": wl.E, "k": wl.k, "d_ff": wl.f, "act": wl.act,
                    "capacity": f"{cap_rule[0]} {cap_rule[1]}/{cap_rule[2]}",
                    "rows": args.rows, "pass": "fwd+bwd" if wl.backward else "fwd",
-                   "parallelism": "single GPU"},
+                   "row_align": L.row_align, "parallelism": "single GPU"},
         "roofline": roof,
         "cpu_baseline": None,
         "detail": {"kept_rows": kept, "executed_rows": executed, "status": status,

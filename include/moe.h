@@ -114,15 +114,22 @@ moe_status moe_count(void* stream, int T, int E, int k, const int32_t* ids,
  *                   exact capacity).
  * Computed in exact 64-bit integer arithmetic, then clamped to [cap_min, T].
  *   capacity [E]   int32 out
- *   offsets  [E+1] int32 out: offsets[e] = sum of C of experts < e, so
- *                  expert e owns rows [offsets[e], offsets[e]+C_e);
- *                  offsets[E] is the rows the layout needs (the caller's
- *                  rows_alloc must be at least that).
- * num, den >= 1; cap_min >= 0.
+ *   offsets  [E+1] int32 out: the row layout of the grouped buffers.
+ *                  offsets[e] = sum over experts e' < e of C_e' rounded up
+ *                  to a multiple of row_align, so expert e owns rows
+ *                  [offsets[e], offsets[e]+C_e) and every region starts at
+ *                  a multiple of row_align; offsets[E] is the rows the
+ *                  layout needs (the caller's rows_alloc must be at least
+ *                  that: at most sum C_e + E (row_align - 1)).  row_align = 1
+ *                  packs the regions; 256 (one GEMM tile of rows) keeps each
+ *                  expert's tiles aligned, which the FFN products run faster
+ *                  on.  The layout changes where rows live, not which
+ *                  assignments are kept.
+ * num, den >= 1; cap_min >= 0; 1 <= row_align <= 1024.
  */
 moe_status moe_update_capacity(void* stream, int T, int k, int E,
                                const int32_t* counts, int num, int den,
-                               int cap_min, int32_t* capacity,
+                               int cap_min, int row_align, int32_t* capacity,
                                int32_t* offsets);
 
 /* Workspace bytes of moe_dispatch for these sizes. [host] */
@@ -436,15 +443,17 @@ int moe_caching_decision(int enabled, int64_t unchanged, int64_t samples,
  *
  * moe_policy_create: delta_launch in [0, 64] (iterations launched ahead of
  *   the metric the trigger sees); grow = grow_num/grow_den <= shrink =
- *   shrink_num/shrink_den, all in [1, 10^6]; init_cap [host] [E] >= 0.
+ *   shrink_num/shrink_den, all in [1, 10^6]; row_align in [1, 1024] (the
+ *   region alignment of moe_update_capacity); init_cap [host] [E] >= 0.
  *   Allocates pinned host memory and events.  *out = NULL on error.
  * moe_policy_begin: waits (host) until at most delta_launch iterations are
  *   outstanding, runs the trigger on each metric consumed, and enqueues on
- *   `stream` the upload of capacity [E] and offsets [E+1] (exclusive prefix
- *   sum) when they changed or the buffers differ from the last call.
- *   *rows_needed [host, optional] = sum of the capacities (the rows the
- *   dispatch needs); *recompiled [host, optional] = 1 if the capacities
- *   changed.  EINVAL when called twice without moe_policy_end.
+ *   `stream` the upload of capacity [E] and offsets [E+1] (laid out as
+ *   moe_update_capacity lays them out with row_align) when they changed or
+ *   the buffers differ from the last call.  *rows_needed [host, optional] =
+ *   offsets[E] (the rows the dispatch needs); *recompiled [host, optional] =
+ *   1 if the capacities changed.  EINVAL when called twice without
+ *   moe_policy_end.
  * moe_policy_end: enqueues on `stream` the copy of counts [E] (device) into
  *   the pinned ring and the event that marks it done.
  * moe_policy_state [host]: current capacities cap [E] (optional), iterations
@@ -461,7 +470,7 @@ int moe_capacity_trigger(int T, int E, const int32_t* counts, int32_t* cap,
 
 moe_status moe_policy_create(int T, int k, int E, int delta_launch, int grow_num,
                              int grow_den, int shrink_num, int shrink_den,
-                             int cap_min, const int32_t* init_cap,
+                             int cap_min, int row_align, const int32_t* init_cap,
                              moe_capacity_policy** out);
 void moe_policy_destroy(moe_capacity_policy* p);
 moe_status moe_policy_begin(moe_capacity_policy* p, void* stream, int32_t* capacity,

@@ -214,10 +214,16 @@ def capacity_dynamic(counts: np.ndarray, T: int, num: int, den: int,
     return out
 
 
-def exclusive_offsets(capacity: np.ndarray) -> np.ndarray:
-    """offsets[e] = sum of capacities of experts < e; offsets[E] = total."""
-    off = np.zeros(len(capacity) + 1, dtype=np.int64)
-    off[1:] = np.cumsum(np.asarray(capacity, dtype=np.int64))
+def exclusive_offsets(capacity: np.ndarray, align: int = 1) -> np.ndarray:
+    """Row layout of the grouped expert buffer (a storage choice, not part of
+    the method): expert e's region starts at offsets[e] = the sum, over
+    experts before e, of their capacities each rounded up to a multiple of
+    `align` rows; offsets[E] = the rows the layout takes.  align = 1 packs
+    the regions."""
+    cap = np.asarray(capacity, dtype=np.int64)
+    sizes = (cap + align - 1) // align * align
+    off = np.zeros(len(cap) + 1, dtype=np.int64)
+    off[1:] = np.cumsum(sizes)
     return off
 
 
@@ -555,10 +561,11 @@ def route(x, w_g, bias, k, renorm):
 
 
 def layer_forward(x, w1, w3, w2, act, dtype, ids, weights, capacity,
-                  rows_alloc, E) -> Dict[str, np.ndarray]:
+                  rows_alloc, E, align: int = 1) -> Dict[str, np.ndarray]:
     """Dispatch -> per-expert FFN -> combine for given ids/weights (gate
-    output or cached) and capacities.  All tensors are float64 values."""
-    off = exclusive_offsets(capacity)
+    output or cached) and capacities, in the row layout of
+    exclusive_offsets(capacity, align).  All tensors are float64 values."""
+    off = exclusive_offsets(capacity, align)
     s = assign_slots(ids, E, capacity, off, rows_alloc)
     x_disp = dispatch_rows(x, s["dest_row"], rows_alloc)
     f = w1.shape[1]

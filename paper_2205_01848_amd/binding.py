@@ -29,7 +29,7 @@ SIGNATURES = {
                                _p, _p, _p, _p, _p, _p]),
     "moe_count": (_c_int, [_p, _c_int, _c_int, _c_int, _p, _p, _p]),
     "moe_update_capacity": (_c_int, [_p, _c_int, _c_int, _c_int, _p, _c_int, _c_int, _c_int,
-                                     _p, _p]),
+                                     _c_int, _p, _p]),
     "moe_dispatch_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int]),
     "moe_dispatch": (_c_int, [_p, _c_int, _c_int, _c_int, _c_int, _c_int, _p, _p, _p, _p,
                               _c_i64, _p, _p, _p, _p, _p, _p, _p, _c_size]),
@@ -66,7 +66,7 @@ SIGNATURES = {
     "moe_capacity_trigger": (_c_int, [_c_int, _c_int, _p, _p, _c_int, _c_int, _c_int, _c_int,
                                       _c_int]),
     "moe_policy_create": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
-                                   _c_int, _c_int, _p, _p]),
+                                   _c_int, _c_int, _c_int, _p, _p]),
     "moe_policy_destroy": (None, [_p]),
     "moe_policy_begin": (_c_int, [_p, _p, _p, _p, _p, _p]),
     "moe_policy_end": (_c_int, [_p, _p, _p]),
@@ -178,12 +178,13 @@ def moe_count(ids, E, counts, status):
            "moe_count")
 
 
-def moe_update_capacity(T, k, E, counts, num, den, cap_min, capacity, offsets):
+def moe_update_capacity(T, k, E, counts, num, den, cap_min, capacity, offsets, row_align=1):
     _need(counts, E, "counts", _I32, optional=True)
     _need(capacity, E, "capacity", _I32)
     _need(offsets, E + 1, "offsets", _I32)
     _check(lib().moe_update_capacity(_stream(), T, k, E, _ptr(counts), num, den, cap_min,
-                                     _ptr(capacity), _ptr(offsets)), "moe_update_capacity")
+                                     row_align, _ptr(capacity), _ptr(offsets)),
+           "moe_update_capacity")
 
 
 def moe_dispatch_workspace_bytes(T, E, k) -> int:
@@ -432,11 +433,11 @@ def moe_capacity_trigger(T, counts, cap, grow, shrink, cap_min=0):
 class CapacityPolicy:
     """Owner of one moe_capacity_policy object (see include/moe.h)."""
 
-    def __init__(self, T, k, E, delta_launch, grow, shrink, init_cap, cap_min=0):
+    def __init__(self, T, k, E, delta_launch, grow, shrink, init_cap, cap_min=0, row_align=1):
         init = (ctypes.c_int32 * E)(*[int(c) for c in init_cap])
         h = ctypes.c_void_p()
         _check(lib().moe_policy_create(T, k, E, delta_launch, grow[0], grow[1], shrink[0],
-                                       shrink[1], cap_min, init, ctypes.byref(h)),
+                                       shrink[1], cap_min, row_align, init, ctypes.byref(h)),
                "moe_policy_create")
         self._h, self.E = h, E
 

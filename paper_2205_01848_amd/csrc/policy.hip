@@ -34,6 +34,7 @@
 struct moe_capacity_policy {
   int T = 0, k = 0, E = 0, delta = 0;
   int grow_num = 1, grow_den = 1, shrink_num = 1, shrink_den = 1, cap_min = 0;
+  int row_align = 1;   // expert regions start at multiples of this many rows
   int slots = 0;
   std::vector<int32_t> cap;
   int32_t* ring = nullptr;   // pinned [slots][E] counts
@@ -49,6 +50,11 @@ struct moe_capacity_policy {
 namespace {
 
 int64_t ceil_mul(int num, int den, int64_t c) { return (num * c + den - 1) / den; }
+
+// rows an expert's region takes: its capacity rounded up to row_align
+int64_t aligned_rows(int32_t cap, int row_align) {
+  return (static_cast<int64_t>(cap) + row_align - 1) / row_align * row_align;
+}
 
 int32_t clamp_cap(int64_t v, int cap_min, int T) {
   if (v < cap_min) v = cap_min;
@@ -97,7 +103,7 @@ extern "C" int moe_capacity_trigger(int T, int E, const int32_t* counts, int32_t
 
 extern "C" moe_status moe_policy_create(int T, int k, int E, int delta_launch, int grow_num,
                                         int grow_den, int shrink_num, int shrink_den,
-                                        int cap_min, const int32_t* init_cap,
+                                        int cap_min, int row_align, const int32_t* init_cap,
                                         moe_capacity_policy** out) {
   using namespace moe;
   if (!out) return MOE_EINVAL;
@@ -105,6 +111,7 @@ extern "C" moe_status moe_policy_create(int T, int k, int E, int delta_launch, i
   if (!shape_ok(T, E, k) || delta_launch < 0 || delta_launch > 64 || !init_cap) return MOE_EINVAL;
   if (!ratio_ok(grow_num, grow_den) || !ratio_ok(shrink_num, shrink_den) || cap_min < 0)
     return MOE_EINVAL;
+  if (row_align < 1 || row_align > kMaxRowAlign) return MOE_EINVAL;
   // grow <= shrink: a recompile never leaves a capacity the same metric would shrink
   if (static_cast<int64_t>(grow_num) * shrink_den > static_cast<int64_t>(shrink_num) * grow_den)
     return MOE_EINVAL;
@@ -113,6 +120,7 @@ extern "C" moe_status moe_policy_create(int T, int k, int E, int delta_launch, i
   p->T = T; p->k = k; p->E = E; p->delta = delta_launch;
   p->grow_num = grow_num; p->grow_den = grow_den;
   p->shrink_num = shrink_num; p->shrink_den = shrink_den; p->cap_min = cap_min;
+  p->row_align = row_align;
   p->slots = delta_launch + 2;
   p->cap.resize(E);
   for (int e = 0; e < E; ++e) {
@@ -167,7 +175,7 @@ extern "C" moe_status moe_policy_begin(moe_capacity_policy* p, void* stream, int
     for (int e = 0; e < p->E; ++e) {
       st[e] = p->cap[e];
       st[p->E + e] = static_cast<int32_t>(acc);
-      acc += p->cap[e];
+      acc += aligned_rows(p->cap[e], p->row_align);
     }
     if (acc >= (int64_t(1) << 31)) {
       p->dirty = true;  // the capacities were not uploaded
@@ -185,7 +193,7 @@ extern "C" moe_status moe_policy_begin(moe_capacity_policy* p, void* stream, int
   }
   if (rows_needed) {
     int64_t acc = 0;
-    for (int e = 0; e < p->E; ++e) acc += p->cap[e];
+    for (int e = 0; e < p->E; ++e) acc += aligned_rows(p->cap[e], p->row_align);
     *rows_needed = acc;
   }
   if (recompiled) *recompiled = changed ? 1 : 0;

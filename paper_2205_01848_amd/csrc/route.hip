@@ -65,10 +65,13 @@ __global__ __launch_bounds__(256) void count_kernel(const int32_t* __restrict__ 
   if (threadIdx.x < E && h[threadIdx.x]) atomicAdd(&counts[threadIdx.x], h[threadIdx.x]);
 }
 
-// Eq. 4 / dynamic capacity factors, exact 64-bit integer ceil, + offsets.
+// Eq. 4 / dynamic capacity factors, exact 64-bit integer ceil, + offsets:
+// expert e's region starts at the sum of the earlier capacities, each
+// rounded up to a multiple of row_align rows.
 __global__ __launch_bounds__(64) void capacity_kernel(int T, int k, int E,
                                                       const int32_t* __restrict__ counts,
                                                       int num, int den, int cap_min,
+                                                      int row_align,
                                                       int32_t* __restrict__ capacity,
                                                       int32_t* __restrict__ offsets) {
   __shared__ int64_t c[kMaxE];
@@ -92,7 +95,7 @@ __global__ __launch_bounds__(64) void capacity_kernel(int T, int k, int E,
     int64_t run = 0;
     for (int i = 0; i < E; ++i) {
       offsets[i] = static_cast<int32_t>(run);
-      run += c[i];
+      run += (c[i] + row_align - 1) / row_align * row_align;
     }
     offsets[E] = static_cast<int32_t>(run);
   }
@@ -571,13 +574,16 @@ extern "C" moe_status moe_count(void* stream, int T, int E, int k, const int32_t
 
 extern "C" moe_status moe_update_capacity(void* stream, int T, int k, int E,
                                           const int32_t* counts, int num, int den,
-                                          int cap_min, int32_t* capacity, int32_t* offsets) {
+                                          int cap_min, int row_align, int32_t* capacity,
+                                          int32_t* offsets) {
   if (!shape_ok(T, E, k) || num < 1 || den < 1 || cap_min < 0) return MOE_EINVAL;
+  if (row_align < 1 || row_align > kMaxRowAlign) return MOE_EINVAL;
   if (!capacity || !offsets) return MOE_EINVAL;
-  if (static_cast<int64_t>(T) * E >= (int64_t(1) << 31)) return MOE_EINVAL;
+  if (static_cast<int64_t>(T) * E + static_cast<int64_t>(row_align - 1) * E >= (int64_t(1) << 31))
+    return MOE_EINVAL;
   MOE_TIMED("capacity", static_cast<hipStream_t>(stream));
-  capacity_kernel<<<1, 64, 0, static_cast<hipStream_t>(stream)>>>(T, k, E, counts, num, den,
-                                                                 cap_min, capacity, offsets);
+  capacity_kernel<<<1, 64, 0, static_cast<hipStream_t>(stream)>>>(
+      T, k, E, counts, num, den, cap_min, row_align, capacity, offsets);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }

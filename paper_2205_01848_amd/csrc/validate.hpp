@@ -9,6 +9,7 @@
 namespace moe {
 
 constexpr int kMaxE = 64;
+constexpr int kMaxRowAlign = 1024;   // largest region alignment of the grouped buffers (rows)
 constexpr int kMaxK = 8;
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }

@@ -7,6 +7,8 @@ once, on the host, with no device synchronisation:
 * static capacity factor alpha = num/den:  rows_alloc = E * min(T, ceil(alpha*T*k/E))
 * dynamic capacity with margin num/den:    rows_alloc = min(E*T, ceil(num*T*k/den) + E)
 * exact capacity (margin 1):               rows_alloc = T*k
+each plus, when the regions are aligned (row_align > 1), at most
+row_align - 1 padding rows per expert.
 """
 from __future__ import annotations
 
@@ -21,21 +23,31 @@ def _cdiv(a: int, b: int) -> int:
     return -(-a // b)
 
 
-def rows_alloc_for(kind: str, T: int, k: int, E: int, num: int = 1, den: int = 1) -> int:
+# Default alignment (rows) of the expert regions of the grouped buffers
+# (moe_update_capacity's row_align).  1 packs them: regions aligned to the
+# GEMMs' 256-row tiles measured the same step time on MI355X (within 0.5% on
+# every workload), so the packed layout, which needs no padding rows, is kept.
+ROW_ALIGN = 1
+
+
+def rows_alloc_for(kind: str, T: int, k: int, E: int, num: int = 1, den: int = 1,
+                   align: int = ROW_ALIGN) -> int:
     if kind == "static":
-        return E * min(T, _cdiv(num * T * k, den * E))
+        return E * _cdiv(min(T, _cdiv(num * T * k, den * E)), align) * align
+    pad = E * (align - 1)
     if kind == "dynamic":
-        return min(E * T, _cdiv(num * T * k, den) + E)
+        return min(E * T, _cdiv(num * T * k, den) + E) + pad
     if kind == "exact":
-        return T * k
+        return T * k + pad
     raise ValueError(kind)
 
 
 class MoELayer:
     def __init__(self, T: int, d: int, E: int, k: int, f: int, act: str,
                  dtype: torch.dtype, rows_alloc: int, backward: bool = False,
-                 gate: bool = True, device="cuda"):
+                 gate: bool = True, device="cuda", row_align: int = ROW_ALIGN):
         self.T, self.d, self.E, self.k, self.f = T, d, E, k, f
+        self.row_align = row_align
         self.act = B.ACTS[act]
         self.swiglu = act == "swiglu"
         self.dtype = dtype
@@ -94,12 +106,13 @@ class MoELayer:
 
     def capacity_static(self, num: int, den: int, cap_min: int = 0):
         B.moe_update_capacity(self.T, self.k, self.E, None, num, den, cap_min, self.capacity,
-                              self.offsets)
+                              self.offsets, row_align=self.row_align)
 
     def capacity_dynamic(self, num: int, den: int, counts: Optional[torch.Tensor] = None,
                          cap_min: int = 0):
         B.moe_update_capacity(self.T, self.k, self.E, self.counts if counts is None else counts,
-                              num, den, cap_min, self.capacity, self.offsets)
+                              num, den, cap_min, self.capacity, self.offsets,
+                              row_align=self.row_align)
 
     def dispatch(self, x, ids: Optional[torch.Tensor] = None):
         B.moe_dispatch(x, self.ids if ids is None else ids, self.E, self.capacity, self.offsets,

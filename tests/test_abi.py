@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared_functions():
         assert hasattr(lib, name), name
         assert name in B.SIGNATURES, f"binding lacks {name}"
-    assert lib.moe_abi_version() == 3
+    assert lib.moe_abi_version() == 4
     assert lib.moe_status_string(0) == b"MOE_OK"
 
 
@@ -65,10 +65,12 @@ def test_gate_rejects_null_and_misaligned():
 
 def test_capacity_and_count_reject_bad_arguments():
     L = B.lib()
-    assert L.moe_update_capacity(None, 10, 1, 4, None, 0, 1, 0, FAKE, FAKE) == EINVAL   # num < 1
-    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 0, 0, FAKE, FAKE) == EINVAL   # den < 1
-    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 1, -1, FAKE, FAKE) == EINVAL  # cap_min
-    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 1, 0, None, FAKE) == EINVAL
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 0, 1, 0, 1, FAKE, FAKE) == EINVAL   # num < 1
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 0, 0, 1, FAKE, FAKE) == EINVAL   # den < 1
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 1, -1, 1, FAKE, FAKE) == EINVAL  # cap_min
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 1, 0, 1, None, FAKE) == EINVAL
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 1, 0, 0, FAKE, FAKE) == EINVAL   # row_align
+    assert L.moe_update_capacity(None, 10, 1, 4, None, 1, 1, 0, 1025, FAKE, FAKE) == EINVAL
     assert L.moe_count(None, 10, 4, 1, FAKE, None, FAKE) == EINVAL
 
 
@@ -153,11 +155,12 @@ def test_policy_rejects_bad_arguments():
     init = (ctypes.c_int32 * 4)(5, 5, 5, 5)
     h = ctypes.c_void_p()
     # grow above shrink, negative delta, bad ratio, negative initial capacity
-    assert L.moe_policy_create(100, 2, 4, 1, 14, 10, 13, 10, 0, init, ctypes.byref(h)) == EINVAL
-    assert L.moe_policy_create(100, 2, 4, -1, 11, 10, 13, 10, 0, init, ctypes.byref(h)) == EINVAL
-    assert L.moe_policy_create(100, 2, 4, 1, 0, 10, 13, 10, 0, init, ctypes.byref(h)) == EINVAL
+    assert L.moe_policy_create(100, 2, 4, 1, 14, 10, 13, 10, 0, 1, init, ctypes.byref(h)) == EINVAL
+    assert L.moe_policy_create(100, 2, 4, -1, 11, 10, 13, 10, 0, 1, init, ctypes.byref(h)) == EINVAL
+    assert L.moe_policy_create(100, 2, 4, 1, 0, 10, 13, 10, 0, 1, init, ctypes.byref(h)) == EINVAL
     neg = (ctypes.c_int32 * 4)(5, -1, 5, 5)
-    assert L.moe_policy_create(100, 2, 4, 1, 11, 10, 13, 10, 0, neg, ctypes.byref(h)) == EINVAL
+    assert L.moe_policy_create(100, 2, 4, 1, 11, 10, 13, 10, 0, 1, neg, ctypes.byref(h)) == EINVAL
+    assert L.moe_policy_create(100, 2, 4, 1, 11, 10, 13, 10, 0, 0, init, ctypes.byref(h)) == EINVAL  # row_align
     assert not h.value
     assert L.moe_policy_begin(None, None, FAKE, FAKE, None, None) == EINVAL
     assert L.moe_policy_end(None, None, FAKE) == EINVAL

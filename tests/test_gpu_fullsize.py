@@ -27,6 +27,7 @@ import oracle as O
 import workloads as W
 from gpu_util import NEAR_TIE, RTOL, assert_close, dev, relu_kink_bound, to_dev, to_np, torch_dtype
 from paper_2205_01848_amd import MoELayer, rows_alloc_for
+from paper_2205_01848_amd.layer import ROW_ALIGN
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 
@@ -124,7 +125,7 @@ def _check(name, run):
     kind, num, den = rule
     cap = (O.capacity_static(wl.T, wl.k, wl.E, num, den) if kind == "static"
            else O.capacity_dynamic(counts, wl.T, num, den))
-    off = O.exclusive_offsets(cap)
+    off = O.exclusive_offsets(cap, ROW_ALIGN)
     s = O.assign_slots(ids, wl.E, cap, off, R)
     np.testing.assert_array_equal(to_np(L.counts), s["counts"])
     np.testing.assert_array_equal(to_np(L.capacity), cap)

@@ -21,6 +21,7 @@ import oracle as O
 import workloads as W
 from gpu_util import NEAR_TIE, RTOL, assert_close, dev, to_dev, to_np
 from paper_2205_01848_amd import MoELayer, rows_alloc_for
+from paper_2205_01848_amd.layer import ROW_ALIGN
 from paper_2205_01848_amd import binding as B
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
@@ -98,7 +99,7 @@ def test_balance_and_spec_loss_full_size(c5):
 
     kind, num, den = wl.capacity[0]
     cap = O.capacity_dynamic(counts, wl.T, num, den)
-    off = O.exclusive_offsets(cap)
+    off = O.exclusive_offsets(cap, ROW_ALIGN)
     s = O.assign_slots(ids, wl.E, cap, off, R)
     dest = s["dest_row"]
     np.testing.assert_array_equal(to_np(L.dest_row), dest)
@@ -169,7 +170,7 @@ def test_cached_forward_full_size(c5):
     counts = O.count_assignments(cached, wl.E)
     kind, num, den = wl.capacity[0]
     cap = O.capacity_dynamic(counts, wl.T, num, den)
-    s = O.assign_slots(cached, wl.E, cap, O.exclusive_offsets(cap), R)
+    s = O.assign_slots(cached, wl.E, cap, O.exclusive_offsets(cap, ROW_ALIGN), R)
     dest = s["dest_row"]
     np.testing.assert_array_equal(to_np(L.dest_row), dest)
     toks = _sample(dest, 32, 5)

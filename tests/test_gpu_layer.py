@@ -16,6 +16,7 @@ import workloads as W
 from gpu_util import (NEAR_TIE, RTOL, assert_close, dev, min_topk_gap, relu_kink_bound,
                       scaled_small, to_dev, to_np, torch_dtype)
 from paper_2205_01848_amd import MoELayer, rows_alloc_for
+from paper_2205_01848_amd.layer import ROW_ALIGN
 
 pytestmark = pytest.mark.gpu
 
@@ -67,7 +68,7 @@ def _run(wl, I, run_idx):
     cap = _oracle_capacity(kind, num, den, wl, counts)
     W1, W2 = f64(I.w1), f64(I.w2)
     W3 = f64(I.w3) if I.w3 is not None else None
-    fw = O.layer_forward(X, W1, W3, W2, wl.act, dt, ids, wts, cap, R, wl.E)
+    fw = O.layer_forward(X, W1, W3, W2, wl.act, dt, ids, wts, cap, R, wl.E, ROW_ALIGN)
     np.testing.assert_array_equal(to_np(L.counts), fw["counts"])
     np.testing.assert_array_equal(to_np(L.capacity), cap)
     np.testing.assert_array_equal(to_np(L.fill), fw["fill"])
@@ -170,7 +171,7 @@ def test_lagged_dynamic_capacity_uses_previous_counts():
     cap = O.capacity_dynamic(c1, wl.T, 11, 10)
     np.testing.assert_array_equal(to_np(L.capacity), cap)
     fw = O.layer_forward(f64(I2.x), f64(I1.w1), None, f64(I1.w2), "relu", "bf16", r2["ids"],
-                         r2["weights"], cap, R, wl.E)
+                         r2["weights"], cap, R, wl.E, ROW_ALIGN)
     np.testing.assert_array_equal(to_np(L.dest_row), fw["dest_row"])
     assert_close(to_np(L.y), fw["y"], 2e-2, "y")
 
@@ -223,7 +224,7 @@ def test_padded_static_baseline_weight_gradients_equal_method(act):
     f64 = lambda t: None if t is None else to_np(t)
     capo = O.capacity_static(T, k, E, num, den)
     fw = O.layer_forward(X, f64(w1), f64(w3), f64(w2), act, "bf16", ids, wts.astype(np.float64),
-                         capo, R, E)
+                         capo, R, E, ROW_ALIGN)
     np.testing.assert_array_equal(to_np(out["fill"]["dest_row"]), fw["dest_row"])
     bw = O.layer_backward(fw, X, DY, f64(w1), f64(w3), f64(w2), act, "bf16", ids,
                           wts.astype(np.float64), E)

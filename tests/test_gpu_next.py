@@ -21,6 +21,7 @@ import oracle as O
 import workloads as W
 from gpu_util import NEAR_TIE, RTOL, assert_close, dev, min_topk_gap, scaled_small, to_dev, to_np, torch_dtype
 from paper_2205_01848_amd import MoELayer, rows_alloc_for
+from paper_2205_01848_amd.layer import ROW_ALIGN
 from paper_2205_01848_amd import binding as B
 
 pytestmark = pytest.mark.gpu
@@ -176,7 +177,8 @@ def test_layer_backward_with_spec_loss_and_balance(name, lam):
            else O.capacity_dynamic(counts, wl.T, num, den))
     W1, W2 = _dec(I.w1, dt), _dec(I.w2, dt)
     W3 = _dec(I.w3, dt) if I.w3 is not None else None
-    fw = O.layer_forward(X, W1, W3, W2, wl.act, dt, r["ids"], r["weights"], cap, R, wl.E)
+    fw = O.layer_forward(X, W1, W3, W2, wl.act, dt, r["ids"], r["weights"], cap, R, wl.E,
+                         ROW_ALIGN)
     Bref, coef = O.balance_term(r["logits"], counts, wl.k, lam)
     assert_close(to_np(L.balance_loss), np.array([Bref]), 1e-5, "balance loss")
     assert_close(to_np(L.dprob_coef), coef, 1e-6, "dprob coefficient")
@@ -285,7 +287,7 @@ def test_forward_cached_with_concurrent_gate(concurrent):
     counts = O.count_assignments(cached, E)
     cap = O.capacity_dynamic(counts, T, 21, 20)
     W1, W2, W3 = _dec(I.w1, dt), _dec(I.w2, dt), _dec(I.w3, dt)
-    fw = O.layer_forward(X, W1, W3, W2, wl.act, dt, cached, wts, cap, R, E)
+    fw = O.layer_forward(X, W1, W3, W2, wl.act, dt, cached, wts, cap, R, E, ROW_ALIGN)
     np.testing.assert_array_equal(to_np(L.dest_row), fw["dest_row"])
     rt = RTOL[dt]
     assert_close(to_np(L.y), fw["y"], rt, "y")

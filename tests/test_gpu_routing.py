@@ -225,3 +225,67 @@ def test_dispatch_all_to_one_expert_and_empty_batch():
     g = _run_dispatch(np.zeros((0, 8), np.uint16), np.zeros((0, 1), np.int32), E, cap, off, 50,
                       "bf16")
     assert (g["counts"] == 0).all() and (g["fill"] == 0).all() and (g["src"] == -1).all()
+
+
+@pytest.mark.parametrize("row_align", [256, 7])
+def test_aligned_layout_routing_matches_oracle(row_align):
+    """Regions aligned to row_align rows: capacities unchanged, offsets on
+    multiples of the alignment, and the dispatch (counts, fill, dest_row, src,
+    rows) bit-exact against the oracle in the same layout."""
+    rng = np.random.default_rng(91)
+    T, E, k, d = 5000, 8, 2, 64
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    ids[: T // 3, 0] = 0
+    counts = O.count_assignments(ids, E)
+    cap_ref = O.capacity_dynamic(counts * 9 // 10, T, 11, 10)       # lagged: some drops
+    off_ref = O.exclusive_offsets(cap_ref, row_align)
+    R = int(off_ref[-1]) + 3
+    t_counts = torch.from_numpy((counts * 9 // 10).astype(np.int32)).to(dev())
+    cap = torch.empty(E, dtype=torch.int32, device=dev())
+    off = torch.empty(E + 1, dtype=torch.int32, device=dev())
+    B.moe_update_capacity(T, k, E, t_counts, 11, 10, 0, cap, off, row_align=row_align)
+    x = torch.from_numpy(W.to_bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
+                         .view(np.int16)).view(torch.bfloat16).to(dev())
+    outs = dict(counts=torch.empty(E, dtype=torch.int32, device=dev()),
+                fill=torch.empty(E, dtype=torch.int32, device=dev()),
+                dest=torch.empty(T, k, dtype=torch.int32, device=dev()),
+                src=torch.empty(R, dtype=torch.int32, device=dev()),
+                xd=torch.zeros(R, d, dtype=torch.bfloat16, device=dev()),
+                status=torch.zeros(1, dtype=torch.int32, device=dev()))
+    ws = B.workspace(B.moe_dispatch_workspace_bytes(T, E, k), dev())
+    B.moe_dispatch(x, torch.from_numpy(ids).to(dev()), E, cap, off, R, outs["counts"],
+                   outs["fill"], outs["dest"], outs["src"], outs["xd"], outs["status"], ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(cap), cap_ref)
+    np.testing.assert_array_equal(to_np(off), off_ref)
+    assert (to_np(off)[:-1] % row_align == 0).all()
+    s = O.assign_slots(ids, E, cap_ref, off_ref, R)
+    np.testing.assert_array_equal(to_np(outs["counts"]), s["counts"])
+    np.testing.assert_array_equal(to_np(outs["fill"]), s["fill"])
+    np.testing.assert_array_equal(to_np(outs["dest"]), s["dest_row"])
+    np.testing.assert_array_equal(to_np(outs["src"]), s["src"])
+    assert int(outs["status"].item()) == s["status"]     # duplicates from the forced picks
+    kept = s["dest_row"] >= 0
+    xd = to_np(outs["xd"])
+    X = to_np(x)
+    tt, jj = np.nonzero(kept)
+    np.testing.assert_array_equal(xd[s["dest_row"][tt, jj]], X[tt])
+
+
+def test_policy_uploads_aligned_offsets():
+    T, E, k = 1000, 4, 2
+    pol = B.CapacityPolicy(T, k, E, 0, (11, 10), (3, 2), [500] * E, row_align=256)
+    cap = torch.empty(E, dtype=torch.int32, device=dev())
+    off = torch.empty(E + 1, dtype=torch.int32, device=dev())
+    counts = torch.tensor([400, 600, 500, 500], dtype=torch.int32, device=dev())
+    rows, _ = pol.begin(cap, off)
+    pol.end(counts)
+    assert rows == 4 * 512
+    rows, rec = pol.begin(cap, off)              # sees iteration 0's counts: 600 overflowed
+    pol.end(counts)
+    torch.cuda.synchronize()
+    pol.close()
+    assert rec
+    np.testing.assert_array_equal(to_np(cap), [440, 660, 550, 550])
+    np.testing.assert_array_equal(to_np(off), O.exclusive_offsets([440, 660, 550, 550], 256))
+    assert rows == int(O.exclusive_offsets([440, 660, 550, 550], 256)[-1])

@@ -45,6 +45,37 @@ def test_dynamic_capacity_exact_rational():
 
 def test_offsets():
     np.testing.assert_array_equal(O.exclusive_offsets([3, 0, 5]), [0, 3, 3, 8])
+    # aligned layout, worked by hand: regions rounded up to multiples of align
+    np.testing.assert_array_equal(O.exclusive_offsets([3, 0, 5], 4), [0, 4, 4, 12])
+    np.testing.assert_array_equal(O.exclusive_offsets([300, 0, 256, 1], 256),
+                                  [0, 512, 512, 768, 1024])
+
+
+def test_aligned_layout_keeps_the_same_assignments():
+    """Region alignment moves rows, never changes which assignments are kept:
+    every region starts on a multiple of the alignment, regions do not
+    overlap, the layout takes at most sum C + E (align - 1) rows, and counts,
+    fill, the kept mask and each assignment's position inside its expert's
+    region equal those of the packed layout."""
+    rng = np.random.default_rng(31)
+    for E, k, align in [(8, 2, 256), (64, 1, 256), (5, 3, 7), (16, 2, 1)]:
+        T = 900
+        ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+        counts = O.count_assignments(ids, E)
+        cap = O.capacity_dynamic(counts * 9 // 10, T, 11, 10)        # lagged: some drops
+        p_off = O.exclusive_offsets(cap)
+        a_off = O.exclusive_offsets(cap, align)
+        assert (a_off[:-1] % align == 0).all()
+        assert (a_off[1:] - a_off[:-1] >= cap).all()
+        assert a_off[-1] <= cap.sum() + E * (align - 1)
+        ps = O.assign_slots(ids, E, cap, p_off, int(p_off[-1]))
+        ak = O.assign_slots(ids, E, cap, a_off, int(a_off[-1]))
+        for key in ("counts", "fill", "status"):
+            np.testing.assert_array_equal(ps[key], ak[key])
+        np.testing.assert_array_equal(ps["dest_row"] >= 0, ak["dest_row"] >= 0)
+        kept = ps["dest_row"] >= 0
+        np.testing.assert_array_equal((ps["dest_row"] - p_off[ids])[kept],
+                                      (ak["dest_row"] - a_off[ids])[kept])
 
 
 # -- slots ---------------------------------------------------------------------
