@@ -1082,10 +1082,12 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
   };
   uint4 f0a[8], f0b[8], f1a[8], f1b[8];   // fragments of k-half 0 / 1 of a stage
 
-  // A wave whose rows or columns of the tile are all beyond the valid ones
-  // skips its reads and MFMAs (it still loads and takes every barrier).
-  bool active = true;
-  if constexpr (!FULL) active = wm * 128 < op.a.rows && wn * (GATED ? 64 : 128) < op.b.rows;
+  // Every wave runs the same instruction stream on every tile: rows, columns
+  // and K past the valid ones were loaded as zeros, so a wave with no valid
+  // rows or columns multiplies zeros, and the epilogue stores none of them.
+  // (Skipping such a wave's reads and MFMAs with a branch per group broke
+  // the interleaving for the whole tile: a partial tile then took several
+  // times as long as a full one.)
 
   // One K step from stage (ca, cb), the next stage in (na, nb); the loads of
   // step kt + 2 go into (ca, cb): its A part once every wave has read the A
@@ -1098,11 +1100,9 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
     // first quarter: MFMAs 0..31 of k-half 0, reads of the A fragments of k-half 1
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
-      if (active) {
-        read1(ca, cb, 1, f1a, f1b, g);
+      read1(ca, cb, 1, f1a, f1b, g);
 #pragma unroll
-        for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f0a[m >> 3], f0b[m & 7]);
-      }
+      for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f0a[m >> 3], f0b[m & 7]);
       __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
@@ -1114,11 +1114,9 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
     for (int g = 8; g < 16; ++g) {
       // A loads 0..5 at groups 8, 9, 11, 12, 14, 15
       if (g % 3 != 1) load1(s, ca, cb, g - 8 - (g - 8) / 3);
-      if (active) {
-        read1(ca, cb, 1, f1a, f1b, g);
+      read1(ca, cb, 1, f1a, f1b, g);
 #pragma unroll
-        for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f0a[m >> 3], f0b[m & 7]);
-      }
+      for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f0a[m >> 3], f0b[m & 7]);
       __builtin_amdgcn_sched_barrier(0);
     }
     // stage kt + 1 has landed (only the 6 A loads just issued may be pending)
@@ -1131,11 +1129,9 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
     for (int g = 0; g < 16; ++g) {
       // A loads 6, 7 and the B loads at groups 0, 2, 3, 5, 6, 8, 9, 11, 12, 14
       if (g % 3 != 1 && g < 15) load1(s, ca, cb, 6 + g - (g + 1) / 3);
-      if (active) {
-        read1(na, nb, 0, f0a, f0b, g);
+      read1(na, nb, 0, f0a, f0b, g);
 #pragma unroll
-        for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f1a[m >> 3], f1b[m & 7]);
-      }
+      for (int m = 4 * g; m < 4 * g + 4; ++m) mfma16(acc[m >> 3][m & 7], f1a[m >> 3], f1b[m & 7]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -1149,10 +1145,8 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
   }
   __builtin_amdgcn_s_waitcnt(0x4F70);   // vmcnt(16): this wave's stage-0 loads landed
   __builtin_amdgcn_s_barrier();
-  if (active) {
 #pragma unroll
-    for (int g = 0; g < 16; ++g) read1(la0, lb0, 0, f0a, f0b, g);
-  }
+  for (int g = 0; g < 16; ++g) read1(la0, lb0, 0, f0a, f0b, g);
   for (int kt = 0; kt < nk2; kt += 2) {
     step(kt, la0, lb0, la1, lb1);
     step(kt + 1, la1, lb1, la0, lb0);
