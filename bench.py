@@ -121,16 +121,29 @@ def blas_gemm(shape, steps, warmup):
     a = torch.randn(M, K, device="cuda:0", dtype=torch.bfloat16, generator=g)
     b = torch.randn(N, K, device="cuda:0", dtype=torch.bfloat16, generator=g)
     c = torch.empty(M, N, device="cuda:0", dtype=torch.bfloat16)
-    for _ in range(warmup):
+    # the clock ramps up over the first few hundred milliseconds of load: warm
+    # up for at least 0.5 s (and `warmup` products), then time at least
+    # `steps` products and 1 s
+    t0 = time.perf_counter()
+    n = 0
+    while n < warmup or time.perf_counter() - t0 < 0.5:
         torch.matmul(a, b.t(), out=c)
+        n += 1
+        if n % 20 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    n = 0
     e0.record()
-    for _ in range(steps):
+    while n < steps or time.perf_counter() - t0 < 1.0:
         torch.matmul(a, b.t(), out=c)
+        n += 1
+        if n % 20 == 0:
+            torch.cuda.synchronize()
     e1.record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
+    ms = e0.elapsed_time(e1) / n
     print(json.dumps({"blas_gemm": [M, N, K], "ms": round(ms, 4),
                       "tflops": round(2.0 * M * N * K / (ms / 1e3) / 1e12, 1),
                       "frac_bf16_peak": round(2.0 * M * N * K / (ms / 1e3) / 1e12 /
