@@ -87,6 +87,11 @@ def parse():
                     help="instead of the layer: time hipBLASLt (torch.matmul) on one bf16 "
                          "product C[M,N] = A[M,K] B[N,K]^T with N(0,1) operands (context: "
                          "an achievable GEMM rate on this GPU; not part of the path)")
+    ap.add_argument("--iso-gemm", default=None, metavar="M,D,F",
+                    help="instead of the layer: the library's two forward products of one "
+                         "ReLU expert (H = X W1^T: M x F x D, Y = A W2^T: M x D x F; no saved "
+                         "planes) and hipBLASLt (torch.matmul) on the same tensors, each "
+                         "sustained for a second after a half-second warm-up")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead of the layer: time a plain device-to-device copy of this "
                          "many GiB (achievable HBM bandwidth; byte-counter calibration)")
@@ -148,6 +153,73 @@ def blas_gemm(shape, steps, warmup):
                       "tflops": round(2.0 * M * N * K / (ms / 1e3) / 1e12, 1),
                       "frac_bf16_peak": round(2.0 * M * N * K / (ms / 1e3) / 1e12 /
                                               PEAK_BF16_TFLOPS, 4)}))
+
+
+def iso_gemm(shape):
+    """The library's forward products of one ReLU expert against hipBLASLt on
+    the same tensors (X ~ N(0,1), W ~ N(0,0.02), bf16)."""
+    import torch
+
+    from paper_2205_01848_amd import binding as B
+    M, d, f = (int(v) for v in shape.split(","))
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(1)
+    x = torch.randn(M, d, device=dev, generator=g).to(torch.bfloat16)
+    w1 = (torch.randn(1, f, d, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+    w2 = (torch.randn(1, d, f, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+    off = torch.tensor([0, M], device=dev, dtype=torch.int32)
+    rows = torch.tensor([M], device=dev, dtype=torch.int32)
+    y = torch.empty(M, d, device=dev, dtype=torch.bfloat16)
+    ws = torch.empty(B.moe_ffn_fwd_workspace_bytes(B.MOE_BF16, B.MOE_RELU, 1, d, f, M),
+                     device=dev, dtype=torch.uint8)
+    h = torch.empty(M, f, device=dev, dtype=torch.bfloat16)
+    yb = torch.empty(M, d, device=dev, dtype=torch.bfloat16)
+
+    def ours():
+        B.moe_expert_ffn_fwd(B.MOE_RELU, off, rows, x, w1, None, w2, None, y, ws)
+
+    def blas():
+        torch.matmul(x, w1[0].t(), out=h)
+        torch.matmul(h, w2[0].t(), out=yb)
+
+    def sustain(fn, timing):
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 0.5:
+            fn()
+            torch.cuda.synchronize()
+        if timing:
+            B.moe_timing_report()
+            B.moe_timing_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n = 0
+        t0 = time.perf_counter()
+        e0.record()
+        while time.perf_counter() - t0 < 1.0:
+            fn()
+            n += 1
+            if n % 4 == 0:
+                torch.cuda.synchronize()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / n
+        rep = None
+        if timing:
+            B.moe_timing_enable(False)
+            rep = B.moe_timing_report()
+        return ms, rep
+
+    fl = 2.0 * M * d * f
+    out = {"iso_gemm": [M, d, f]}
+    ms, _ = sustain(blas, False)
+    out["hipblaslt_ms"] = round(ms, 4)
+    out["hipblaslt_tflops"] = round(2 * fl / (ms / 1e3) / 1e12, 1)
+    ms, rep = sustain(ours, True)
+    out["ours_ms"] = round(ms, 4)
+    out["ours_tflops"] = round(2 * fl / (ms / 1e3) / 1e12, 1)
+    for k in ("gemm_fwd_h", "gemm_fwd_y"):
+        c, t = rep[k]
+        out[k + "_tflops"] = round(fl / (t / c / 1e3) / 1e12, 1)
+    print(json.dumps(out))
 
 
 def gemm_flops(wl, kept):
@@ -539,6 +611,9 @@ def main():
         return
     if args.blas_gemm:
         blas_gemm(args.blas_gemm, args.steps, args.warmup)
+        return
+    if args.iso_gemm:
+        iso_gemm(args.iso_gemm)
         return
     if args.policy_sweep:
         policy_sweep(args)

@@ -170,6 +170,19 @@ def counters_main(a):
             else:
                 cells.append(f"{v:.3f}")
         lines.append(f"| {n[:60]} | " + " | ".join(cells) + " |")
+    mix = [n for n in keep[:a.top] if tab[n].get("SQ_INSTS_MFMA")]
+    if mix:
+        cols = [("SQ_INSTS_VALU", "VALU (MFMA included)"), ("SQ_INSTS_SALU", "SALU"),
+                ("SQ_INSTS_VMEM_RD", "VMEM reads"), ("SQ_INSTS_LDS_LOAD", "LDS loads"),
+                ("SQ_INSTS_LDS_STORE", "LDS stores"), ("SQ_INSTS", "all")]
+        lines += ["", "Instructions per MFMA instruction (SQ_INSTS_* / SQ_INSTS_MFMA):", "",
+                  "| kernel | MFMA (M) | " + " | ".join(h for _, h in cols) + " |",
+                  "|---" * (len(cols) + 2) + "|"]
+        for n in mix:
+            row = tab[n]
+            mf = row["SQ_INSTS_MFMA"]
+            cells = [f"{row[c] / mf:.3f}" if c in row else "" for c, _ in cols]
+            lines.append(f"| {n[:60]} | {mf / 1e6:.1f} | " + " | ".join(cells) + " |")
     lines += ["", f"Kernel sources hash: {out['source_hash']}", ""]
     with open(a.out, "w") as f:
         f.write("\n".join(lines))
