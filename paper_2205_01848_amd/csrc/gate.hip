@@ -3,10 +3,13 @@
 //
 // bf16 forward: one workgroup scores 32 tokens against up to 64 experts with
 // v_mfma_f32_32x32x16_bf16 (token rows as the A operand, expert rows of w_g
-// as the B operand, both K-contiguous), its four waves splitting K; x is
-// streamed from HBM exactly once, so the kernel is HBM-bound.
+// as the B operand, both K-contiguous), its four waves splitting K; for rows
+// longer than 2048 and at most 8 experts a second kernel streams whole rows
+// and forms the dot products with v_dot2.  Either way x is streamed from HBM
+// exactly once, so the gate is HBM-bound.
 // fp32 forward: one thread per token with float32 FMAs (small layers only).
 
+#include <algorithm>
 #include <type_traits>
 
 #include "common.hpp"
@@ -227,6 +230,167 @@ inline int gate_split(int T) {
   return S;
 }
 
+// Whole-row bf16 gate for long rows and few experts (2048 < d <= 4096,
+// E <= 8).  Read a cache line at a time from 32 rows of 8 KB at once, as
+// the tiled kernel does, x streams at about 4.6 TB/s; read front to back a
+// row at a time it streams at about 5.7.  Each wave scores a group of
+// TPW = 4 consecutive tokens at a time, in NCH chunks of 1 KB per row: one
+// 16-byte load per lane covers a contiguous kilobyte.  w_g sits in LDS
+// (experts padded to 8 rows, columns to NCH chunks, both with zeros); lane
+// l keeps the partial dot products of its 8 columns of every chunk for all
+// 4 x 8 (token, expert) pairs, with v_dot2 (bf16 pairs, fp32 accumulation),
+// and a butterfly over the lanes gives the group's 32 sums.  While a group
+// is consumed chunk by chunk the same registers are refilled with the
+// wave's next group, so one group (4 * NCH KB) stays in flight per wave;
+// every load is issued (out-of-range lanes read zeros) and the loops have
+// no branch but their own.  The logits of a batch of 32 tokens collect in
+// the wave's LDS, then 32 lanes finish one token each.
+// Sum of value (lane >> 1) of v[0..31] over all 64 lanes, in lanes lane and
+// lane ^ 1.  Each step pairs a lane with a partner that holds the same
+// subset of values, keeps one half of that subset (the upper half in the
+// lane whose distinguishing bit is set) and adds the partner's copy of it:
+// partners lane ^ 32 and lane ^ 16 through the permlane swaps (which move
+// half of each of two registers, so no select is needed), then lane ^ 8
+// (row_ror:8), 7 - lane within 8 lanes (row_half_mirror), lane ^ 2 and
+// lane ^ 1 (quad_perm) through DPP.
+template <int CTRL> __device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float butterfly32(const float (&v)[32], int lane) {
+  float a[16], b[8], c[4], e[2];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]), __float_as_uint(v[i + 16]),
+                                                    false, false);
+    a[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a[i]), __float_as_uint(a[i + 8]),
+                                                    false, false);
+    b[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  const bool u8 = (lane & 8) != 0, u4 = (lane & 4) != 0, u2 = (lane & 2) != 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    c[i] = (u8 ? b[i + 4] : b[i]) + dpp<0x128>(u8 ? b[i] : b[i + 4]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+    e[i] = (u4 ? c[i + 2] : c[i]) + dpp<0x141>(u4 ? c[i] : c[i + 2]);
+  const float f = (u2 ? e[1] : e[0]) + dpp<0x4E>(u2 ? e[0] : e[1]);
+  return f + dpp<0xB1>(f);
+}
+
+constexpr int kRowsChunk = 512;      // bf16 elements per chunk (64 lanes x 8)
+constexpr int kRowsE = 8;            // experts (padded)
+constexpr int kRowsTPW = 4;          // tokens per group: kRowsTPW * kRowsE = 32 values
+constexpr int kRowsBatch = 32;       // tokens finished together
+constexpr int kRowsMinChunks = 5;    // the tiled kernel is as fast up to d = 2048
+constexpr int kRowsMaxChunks = 8;    // w_g in LDS: 8 x 8 KB
+
+template <int NCH>
+__global__ __launch_bounds__(256, 2) void gate_rows_bf16_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wg,
+    const float* __restrict__ bias, int T, int d, int E, int k, int renorm,
+    float* __restrict__ logits, int32_t* __restrict__ ids, float* __restrict__ weights) {
+  constexpr int EC = kRowsE, TPW = kRowsTPW;
+  constexpr int FB = kRowsBatch / TPW;           // groups per batch
+  constexpr int CPR = NCH * 64;                  // 16-byte chunks per LDS row
+  static_assert(TPW * EC == 32, "32 values per lane");
+  __shared__ uint4 wl[EC * CPR];
+  __shared__ float fin[4][kRowsBatch * EC];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int ngroups = (T + TPW - 1) / TPW;
+  const int gw = blockIdx.x * 4 + wave, nw = gridDim.x * 4;
+  const uint32_t rowb = static_cast<uint32_t>(d) * 2;
+
+  // w_g into LDS (rows past E and columns past d read zeros)
+  {
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(wg), static_cast<short>(0), E * rowb, 0x00020000);
+    constexpr int kPer = EC * CPR / 256;
+    uint4 v[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int i = threadIdx.x + j * 256;
+      const int e = i / CPR, c = i - e * CPR;
+      const uint32_t off = (e * rowb + c * 16) | (static_cast<uint32_t>(c * 8 >= d) << 31);
+      v[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rw, off, 0, 0));
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) wl[threadIdx.x + j * 256] = v[j];
+  }
+  uint4 ring[NCH][TPW];
+  // group g's chunk c into slot: bit 31 set (out of range) past the last
+  // group, past T or past d, as arithmetic rather than a branch
+  auto issue = [&](int g, int c, uint4 (&slot)[TPW]) {
+    const __amdgpu_buffer_rsrc_t rx =
+        gate_rsrc(x + static_cast<size_t>(g < ngroups ? g : 0) * TPW * d);
+    const int col = c * kRowsChunk + lane * 8;
+    const uint32_t cbad = static_cast<uint32_t>(col >= d) << 31;
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      const uint32_t rbad = static_cast<uint32_t>(g * TPW + t >= T) << 31;   // also g >= ngroups
+      const uint32_t off = (t * rowb + static_cast<uint32_t>(col) * 2) | cbad | rbad;
+      slot[t] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
+    }
+  };
+  // the wave's groups are gw, gw + nw, ...
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    issue(gw, c, ring[c]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // the (token, expert) value this lane pair ends up with, and its bias
+  const int idx = lane >> 1, ve = idx % EC, vt = idx / EC;
+  const float lane_bias = bias != nullptr && ve < E ? bias[ve] : 0.f;
+  float* my = fin[wave];
+  __syncthreads();
+
+  auto dot8 = [](const uint4& p, const uint4& q, float c) {
+    c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p.x), __builtin_bit_cast(bf16x2, q.x), c, false);
+    c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p.y), __builtin_bit_cast(bf16x2, q.y), c, false);
+    c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p.z), __builtin_bit_cast(bf16x2, q.z), c, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p.w), __builtin_bit_cast(bf16x2, q.w), c, false);
+  };
+  // batches of FB groups: gb, gb + nw, ..., gb + (FB - 1) * nw
+  for (int gb = gw; gb < ngroups; gb += FB * nw) {
+#pragma unroll 1
+    for (int s = 0; s < FB && gb + s * nw < ngroups; ++s) {
+      const int g = gb + s * nw;
+      // w_g is read from LDS again for every group: held in registers
+      // across groups it would take EC * NCH * 4 of them
+      asm volatile("" ::: "memory");
+      float v[32];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) v[i] = 0.f;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const uint4* wc = wl + c * 64 + lane;
+#pragma unroll
+        for (int e = 0; e < EC; ++e) {
+          const uint4 w = wc[e * CPR];
+#pragma unroll
+          for (int t = 0; t < TPW; ++t) v[t * EC + e] = dot8(ring[c][t], w, v[t * EC + e]);
+        }
+        issue(g + nw, c, ring[c]);   // consumed: the wave's next group
+      }
+      const float l = butterfly32(v, lane) + lane_bias;
+      const int tok = g * TPW + vt;
+      if ((lane & 1) == 0) my[s * 32 + idx] = l;
+      if ((lane & 1) == 0 && ve < E && tok < T) logits[static_cast<size_t>(tok) * E + ve] = l;
+    }
+    // token slot lane = (group s, token t) of the batch, its logits at lane * EC
+    __builtin_amdgcn_wave_barrier();
+    const int tok = (gb + (lane / TPW) * nw) * TPW + lane % TPW;
+    if (lane < kRowsBatch && tok < T)
+      finish_token(my + lane * EC, E, k, renorm, ids + static_cast<size_t>(tok) * k,
+                   weights + static_cast<size_t>(tok) * k);
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
 __global__ __launch_bounds__(64) void gate_fwd_f32_kernel(
     const float* __restrict__ x, const float* __restrict__ wg,
     const float* __restrict__ bias, int T, int d, int E, int k, int renorm,
@@ -410,7 +574,23 @@ extern "C" moe_status moe_gate_topk(void* stream, moe_dtype dt, int T, int d,
     return MOE_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   MOE_TIMED("gate_fwd", s);
-  if (dt == MOE_BF16) {
+  const int nch = (d + kRowsChunk - 1) / kRowsChunk;
+  if (dt == MOE_BF16 && E <= kRowsE && nch >= kRowsMinChunks && nch <= kRowsMaxChunks) {
+    // long rows, few experts: whole-row streaming, two workgroups per CU
+    const int groups = (T + kRowsTPW - 1) / kRowsTPW;
+    const int grid = std::min(2 * num_cus(), (groups + 3) / 4);
+    auto go = [&](auto nc) {
+      gate_rows_bf16_kernel<decltype(nc)::value><<<grid, 256, 0, s>>>(
+          static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_g), bias, T, d, E, k,
+          renorm, logits, ids, weights);
+    };
+    switch (nch) {
+      case 5: go(std::integral_constant<int, 5>{}); break;
+      case 6: go(std::integral_constant<int, 6>{}); break;
+      case 7: go(std::integral_constant<int, 7>{}); break;
+      default: go(std::integral_constant<int, 8>{}); break;
+    }
+  } else if (dt == MOE_BF16) {
     const int S = gate_split(T);
     const int tok_per_block = kGateTile * (kGateWaves / S);
     dim3 grid((T + tok_per_block - 1) / tok_per_block);

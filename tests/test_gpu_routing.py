@@ -39,6 +39,18 @@ def _run_gate(x_np, wg_np, b_np, k, renorm, dt):
     # long batches: two waves per token tile, then one (whole rows per wave)
     (40001, 72, 8, 2, 1, "bf16"),
     (70001, 136, 40, 2, 1, "bf16"),
+    # E <= 8 and 2048 < d <= 4096: the whole-row kernel (5 to 8 chunks of
+    # 512 columns), ragged column tails, ragged 4-token groups and 32-token
+    # batches, fewer tokens than waves
+    (5003, 4096, 8, 2, 1, "bf16"),
+    (2049, 2600, 5, 2, 1, "bf16"),
+    (64, 2056, 8, 1, 0, "bf16"),
+    (9, 3584, 3, 3, 1, "bf16"),
+    (20001, 3072, 2, 2, 0, "bf16"),
+    # just past its limits: the tiled kernel
+    (300, 4104, 8, 2, 1, "bf16"),
+    (250, 2056, 9, 2, 0, "bf16"),
+    (777, 1800, 12, 3, 0, "bf16"),
     (129, 64, 4, 1, 0, "f32"),
     (300, 40, 64, 4, 1, "f32"),
 ])
