@@ -92,6 +92,11 @@ def parse():
                          "ReLU expert (H = X W1^T: M x F x D, Y = A W2^T: M x D x F; no saved "
                          "planes) and hipBLASLt (torch.matmul) on the same tensors, each "
                          "sustained for a second after a half-second warm-up")
+    ap.add_argument("--gate-alone", action="store_true",
+                    help="instead of the layer: the gate forward on the workload's shapes, "
+                         "sustained for a second, alone and after writing (or reading) as many "
+                         "bytes as x elsewhere in memory (shows what the previous kernel's "
+                         "dirty cache lines cost the next one)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead of the layer: time a plain device-to-device copy of this "
                          "many GiB (achievable HBM bandwidth; byte-counter calibration)")
@@ -219,6 +224,52 @@ def iso_gemm(shape):
     for k in ("gemm_fwd_h", "gemm_fwd_y"):
         c, t = rep[k]
         out[k + "_tflops"] = round(fl / (t / c / 1e3) / 1e12, 1)
+    print(json.dumps(out))
+
+
+def gate_alone(name):
+    """Gate forward time on the workload's shapes (x ~ N(0,1), w_g ~ N(0,0.02)),
+    alone and after another kernel writes or reads as many bytes as x."""
+    import torch
+
+    import workloads as W
+    from paper_2205_01848_amd import binding as B
+    wl = W.config(name)
+    assert wl.gate == "linear", "the workload has no gate"
+    T, d, E, k = wl.T, wl.d, wl.E, wl.k
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(1)
+    x = torch.randn(T, d, device=dev, generator=g).to(torch.bfloat16)
+    wg = (torch.randn(E, d, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+    bias = torch.zeros(E, device=dev, dtype=torch.float32)
+    logits = torch.empty(T, E, device=dev, dtype=torch.float32)
+    ids = torch.empty(T, k, device=dev, dtype=torch.int32)
+    wts = torch.empty(T, k, device=dev, dtype=torch.float32)
+    other = torch.empty(T, d, device=dev, dtype=torch.bfloat16)
+    before = {"alone": lambda: None,
+              "after_write_of_x_bytes": lambda: other.fill_(1.0),
+              "after_read_of_x_bytes": lambda: torch.sum(other, dtype=torch.float32)}
+    nbytes = T * d * 2 + E * d * 2 + T * E * 4 + T * k * 8
+    out = {"gate_alone": name, "T": T, "d": d, "E": E, "algorithmic_bytes": nbytes}
+    for label, pre in before.items():
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 0.3:
+            pre()
+            B.moe_gate_topk(x, wg, bias, k, wl.renorm, logits, ids, wts)
+            torch.cuda.synchronize()
+        B.moe_timing_report()
+        B.moe_timing_enable(True)
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 1.0:
+            for _ in range(10):
+                pre()
+                B.moe_gate_topk(x, wg, bias, k, wl.renorm, logits, ids, wts)
+            torch.cuda.synchronize()
+        B.moe_timing_enable(False)
+        n, ms = B.moe_timing_report()["gate_fwd"]
+        us = ms / n * 1e3
+        out[label] = {"us": round(us, 2), "GBps": round(nbytes / us / 1e3, 1),
+                      "frac_hbm": round(nbytes / us / 1e3 / PEAK_HBM_GBS, 4), "launches": n}
     print(json.dumps(out))
 
 
@@ -614,6 +665,9 @@ def main():
         return
     if args.iso_gemm:
         iso_gemm(args.iso_gemm)
+        return
+    if args.gate_alone:
+        gate_alone(args.workload)
         return
     if args.policy_sweep:
         policy_sweep(args)

@@ -206,10 +206,11 @@ size_t moe_ffn_bwd_workspace_bytes(moe_dtype dt, moe_act act, int E, int d,
  *   offsets [E+1], rows [E] int32 (rows = fill: the method; rows = capacity:
  *           a padded static-shape baseline)
  *   x_disp  [rows_alloc,d], w1/w3 [E,f,d] (w3 NULL unless SwiGLU), w2 [E,d,f]
- *   h_save  NULL for inference, else out: the planes H, A
- *           [2,rows_alloc,f], or for SwiGLU H1, H3, A [3,rows_alloc,f]
- *           (A = act(H) as the second product consumed it);
- *           moe_expert_ffn_bwd reads it.
+ *   h_save  NULL for inference, else out: the planes moe_expert_ffn_bwd
+ *           reads, each [rows_alloc,f]: ReLU A [1,rows_alloc,f]
+ *           (relu'(H) = [A > 0], so H is not kept), GELU H, A
+ *           [2,rows_alloc,f], SwiGLU H1, H3, A [3,rows_alloc,f] (A = act(H)
+ *           as the second product consumed it).
  *   y_disp  [rows_alloc,d] out.  Rows outside every expert's rows are left
  *           untouched.
  */
@@ -271,7 +272,7 @@ moe_status moe_combine_bwd(void* stream, moe_dtype dt, int T, int d, int k,
  *   (bf16 layers round dH, dH1, dH3);
  *   dw2_e = dY^T A,  dw1_e = dH1^T X,  dw3_e = dH3^T X  (float32; an expert
  *   with no rows gets zeros);  dx_disp = dH1 w1_e + dH3 w3_e (one rounding).
- *   h_save   as written by moe_expert_ffn_fwd (H or H1/H3, and A)
+ *   h_save   as written by moe_expert_ffn_fwd (A; H and A; or H1, H3 and A)
  *   dy_disp  [rows_alloc,d] (moe_combine_bwd output)
  *   dx_disp  [rows_alloc,d] out (rows outside every expert's rows untouched)
  *   dw1 [E,f,d], dw3 [E,f,d] (NULL unless SwiGLU), dw2 [E,d,f] float32 out,

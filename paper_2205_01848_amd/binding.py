@@ -78,6 +78,9 @@ SIGNATURES = {
 _lib = None
 
 
+ABI_VERSION = 5   # moe_abi_version() of the library this binding is written for
+
+
 class MoEError(RuntimeError):
     pass
 
@@ -94,6 +97,11 @@ def lib():
             fn = getattr(L, name)
             fn.restype = res
             fn.argtypes = args
+        # buffer sizes here follow this ABI (h_save planes, argument lists):
+        # a library of another version would read and write past them
+        if L.moe_abi_version() != ABI_VERSION:
+            raise MoEError(f"{LIB_PATH} has ABI version {L.moe_abi_version()}, this binding "
+                           f"expects {ABI_VERSION}: rebuild it (python -m paper_2205_01848_amd.build)")
         _lib = L
     return _lib
 
@@ -146,9 +154,10 @@ def _nbytes(t: torch.Tensor) -> int:
     return t.numel() * t.element_size()
 
 
-def _planes(act: int) -> int:
-    """[rows_alloc, f] planes of h_save: H, A; or H1, H3, A for SwiGLU."""
-    return 3 if act == MOE_SWIGLU else 2
+def h_save_planes(act: int) -> int:
+    """[rows_alloc, f] planes of h_save: A for ReLU, H and A for GELU, H1, H3
+    and A for SwiGLU."""
+    return 3 if act == MOE_SWIGLU else 2 if act == MOE_GELU_TANH else 1
 
 
 def workspace(nbytes: int, device) -> torch.Tensor:
@@ -244,7 +253,7 @@ def moe_expert_ffn_fwd(act, offsets, rows, x_disp, w1, w3, w2, h_save, y_disp, w
     _need(x_disp, R * d, "x_disp", dt)
     _need(w3, E * f * d, "w3", dt, optional=act != MOE_SWIGLU)
     _need(w2, E * d * f, "w2", dt)
-    _need(h_save, _planes(act) * R * f, "h_save", dt, optional=True)
+    _need(h_save, h_save_planes(act) * R * f, "h_save", dt, optional=True)
     _need(y_disp, R * d, "y_disp", dt)
     _check(lib().moe_expert_ffn_fwd(_stream(), _dt(w1), act, E, d, f, _ptr(offsets), _ptr(rows),
                                     x_disp.shape[0], _ptr(x_disp), _ptr(w1), _ptr(w3), _ptr(w2),
@@ -295,7 +304,7 @@ def moe_expert_ffn_bwd(act, offsets, rows, x_disp, h_save, w1, w3, w2, dy_disp, 
     _need(offsets, E + 1, "offsets", _I32)
     _need(rows, E, "rows", _I32)
     _need(x_disp, R * d, "x_disp", dt)
-    _need(h_save, _planes(act) * R * f, "h_save", dt)
+    _need(h_save, h_save_planes(act) * R * f, "h_save", dt)
     _need(w3, E * f * d, "w3", dt, optional=not sw)
     _need(w2, E * d * f, "w2", dt)
     _need(dy_disp, R * d, "dy_disp", dt)

@@ -1460,6 +1460,10 @@ int persistent_grid() {
 
 inline int cdiv(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
 
+// [rows_alloc, f] planes of h_save: A (ReLU), H and A (GELU), H1, H3 and A
+// (SwiGLU).
+int h_save_planes(moe_act act) { return act == MOE_SWIGLU ? 3 : act == MOE_GELU_TANH ? 2 : 1; }
+
 // Sizes of the schedule and of every workspace buffer.
 struct FfnPlan {
   int E, d, f, F;            // F = f (relu/gelu) or 2f (swiglu)
@@ -1610,8 +1614,10 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   const int64_t es = static_cast<int64_t>(pl.es);
   const int64_t plane = rows_alloc * f * es;   // one [rows_alloc, f] plane of h_save
   const bool sw = act == MOE_SWIGLU;
-  // A = act(H): the last plane of h_save when the caller keeps activations
-  char* abuf = h_save ? static_cast<char*>(h_save) + (sw ? 2 : 1) * plane : ws + pl.o_abuf;
+  // A = act(H): the last plane of h_save when the caller keeps activations.
+  // ReLU keeps A alone (relu'(H) = [A > 0]), so H is never written there.
+  const int h_planes = h_save_planes(act) - 1;
+  char* abuf = h_save ? static_cast<char*>(h_save) + h_planes * plane : ws + pl.o_abuf;
 
   GemmParams p = base_params(pl, offsets, ws);
   p.A = static_cast<const char*>(x_disp);
@@ -1625,8 +1631,8 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   p.act = act == MOE_RELU ? ACT_RELU : (act == MOE_GELU_TANH ? ACT_GELU : ACT_SWIGLU);
   p.C = abuf;
   p.ldc = f * es;
-  p.H1 = static_cast<char*>(h_save);
-  p.H3 = h_save ? static_cast<char*>(h_save) + plane : nullptr;
+  p.H1 = h_planes > 0 ? static_cast<char*>(h_save) : nullptr;
+  p.H3 = h_save && sw ? static_cast<char*>(h_save) + plane : nullptr;
   p.ldh = f * es;
   if (sw) {
     p.ntiles = cdiv(f, BN / 2);
@@ -1678,9 +1684,11 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   char* dh = ws + pl.o_dh;      // [rows_alloc, F]: dH, or [dH1 | dH3]
   const int actc = act == MOE_RELU ? ACT_RELU : (act == MOE_GELU_TANH ? ACT_GELU : ACT_SWIGLU);
   const int64_t plane = rows_alloc * f * es;
-  const char* h1 = static_cast<const char*>(h_save);
+  // A = act(H), saved by the forward after H (or H1, H3); ReLU saves A alone
+  // and its derivative reads A: relu'(H) = [H > 0] = [A > 0]
+  const char* abuf = static_cast<const char*>(h_save) + (h_save_planes(act) - 1) * plane;
+  const char* h1 = act == MOE_RELU ? abuf : static_cast<const char*>(h_save);
   const char* h3 = sw ? h1 + plane : nullptr;
-  const char* abuf = h1 + (sw ? 2 : 1) * plane;   // A = act(H), saved by the forward
 
   // dx_disp = [dH1 | dH3] [W1; W3] (W1, W3 read K-major, W3 from k = f on)
   auto launch_dx = [&]() -> moe_status {

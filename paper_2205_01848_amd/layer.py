@@ -76,8 +76,8 @@ class MoELayer:
         self.backward_enabled = backward
         self.h_save = None
         if backward:
-            # H (or H1, H3) and A = act(H), kept for the backward
-            self.h_save = e((3 if self.swiglu else 2) * max(R, 1) * f)
+            # A = act(H), after H (GELU) or H1, H3 (SwiGLU), kept for the backward
+            self.h_save = e(B.h_save_planes(self.act) * max(R, 1) * f)
             self.dy_disp = e(max(R, 1), d)
             self.dx_disp = e(max(R, 1), d)
             self.dweights = e(T, k, t=f32)

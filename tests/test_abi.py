@@ -34,8 +34,18 @@ def test_library_exports_every_declared_symbol():
     for name in declared_functions():
         assert hasattr(lib, name), name
         assert name in B.SIGNATURES, f"binding lacks {name}"
-    assert lib.moe_abi_version() == 4
+    assert lib.moe_abi_version() == B.ABI_VERSION == 5
     assert lib.moe_status_string(0) == b"MOE_OK"
+
+
+def test_binding_refuses_a_library_of_another_abi(monkeypatch):
+    # the binding sizes buffers for its own ABI: an older or newer library
+    # must not be called through it
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "ABI_VERSION", B.ABI_VERSION - 1)
+    with pytest.raises(B.MoEError, match="ABI version"):
+        B.lib()
+    monkeypatch.setattr(B, "_lib", None)
 
 
 FAKE = ctypes.c_void_p(1 << 20)   # never dereferenced: every call below fails validation

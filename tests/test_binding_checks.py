@@ -39,8 +39,13 @@ def test_sizes_that_fit_reach_the_device_check():
 def test_swiglu_h_save_needs_three_planes():
     with pytest.raises(B.MoEError, match="h_save holds"):
         B.moe_expert_ffn_fwd(**_ffn_fwd_args(planes=2))
-    # two planes are enough without SwiGLU
-    a = _ffn_fwd_args(act=B.MOE_RELU, planes=2)
+    # GELU keeps H and A, ReLU only A
+    a = _ffn_fwd_args(act=B.MOE_GELU_TANH, planes=2)
+    a["w3"] = None
+    passes_checks(B.moe_expert_ffn_fwd, **a)
+    with pytest.raises(B.MoEError, match="h_save holds"):
+        B.moe_expert_ffn_fwd(**dict(a, h_save=z(1 * 32 * 16, bf16)))
+    a = _ffn_fwd_args(act=B.MOE_RELU, planes=1)
     a["w3"] = None
     passes_checks(B.moe_expert_ffn_fwd, **a)
 
