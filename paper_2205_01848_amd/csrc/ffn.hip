@@ -118,7 +118,9 @@ template <typename T> struct Raw8 {
 // hardware base-2 exponential and reciprocal (relative error about 1e-6,
 // far below the bf16 rounding of the stored results):
 //   e^x = 2^(x log2 e),  sigmoid(h) = 1 / (1 + e^-h),
-//   tanh(u) = 1 - 2 / (1 + e^(2u))  (both limits exact: e^(2u) -> inf or 0).
+//   tanh(u) = 1 - 2 / (1 + e^(2u))  (both limits exact: e^(2u) -> inf or 0),
+//   and GELU as h sigmoid(2u) (limits: -0 for large negative h, where the
+//   exponential overflows to inf, and h for large positive h).
 __device__ __forceinline__ float exp_fast(float x) {
   return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
 }
@@ -128,9 +130,11 @@ __device__ __forceinline__ float tanh_fast(float u) {
 }
 __device__ __forceinline__ float act_f(float h, int act) {
   if (act == ACT_RELU) return fmaxf(h, 0.f);
-  // GELU, tanh form
-  const float u = 0.7978845608028654f * (h + 0.044715f * h * h * h);
-  return 0.5f * h * (1.f + tanh_fast(u));
+  // GELU, tanh form: 0.5 h (1 + tanh(u)) = h sigmoid(2u) = h / (1 + e^(-2u)),
+  // u = sqrt(2/pi) (h + 0.044715 h^3); -2u log2(e) = h (c1 + c3 h^2)
+  constexpr float c1 = -2.f * 0.7978845608028654f * 1.4426950408889634f;
+  constexpr float c3 = c1 * 0.044715f;
+  return h * rcp_fast(1.f + __builtin_amdgcn_exp2f(h * __builtin_fmaf(c3, h * h, c1)));
 }
 __device__ __forceinline__ float act_grad_f(float h, int act) {
   if (act == ACT_RELU) return h > 0.f ? 1.f : 0.f;

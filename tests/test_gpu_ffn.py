@@ -132,6 +132,24 @@ def test_gelu_swiglu_random(act, dt, case):
     _compare(g, valid, fw, bw, act, dt, exact=False)
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_gelu_large_preactivations(dt):
+    """Pre-activations far into both tails (|H| up to about 60): the kernels'
+    GELU goes through an exponential that overflows to inf on the negative
+    side and must give -0 there, and H itself on the positive side."""
+    E, d, f = 2, 64, 136
+    rows, cap, off, R, P = _problem(E, d, f, [70, 130], [1, 0], "gelu_tanh", dt, False, 50)
+    scale = np.linspace(0.1, 40.0, f)[None, :, None]      # column j of H scaled by scale[j]
+    P["w1"] = _enc(_dec(P["w1"], dt) * scale, dt)
+    valid, fw, bw = _oracle(rows, off, P, "gelu_tanh", dt, E)
+    assert np.abs(fw["H"]).max() > 40 and fw["H"].min() < -40
+    g = _gpu(rows, cap, off, R, P, "gelu_tanh", dt, E, d, f)
+    _compare(g, valid, fw, bw, "gelu_tanh", dt, exact=False)
+    a = g["h"][-1][valid]
+    assert np.isfinite(a).all()
+    assert (a[fw["H"] < -20] == 0).all()
+
+
 def test_split_k_weight_gradients_skewed_experts():
     """One expert holds almost every row, so the dW products split K into
     chunks and add the partial sums in a fixed order."""
