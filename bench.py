@@ -97,6 +97,9 @@ def parse():
                          "sustained for a second, alone and after writing (or reading) as many "
                          "bytes as x elsewhere in memory (shows what the previous kernel's "
                          "dirty cache lines cost the next one)")
+    ap.add_argument("--tiles", type=int, default=0, choices=[0, 1, 2],
+                    help="bf16 GEMM tiles: 0 the library's choice per product, 1 256x256 "
+                         "only, 2 128x128 only (two workgroups per CU)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead of the layer: time a plain device-to-device copy of this "
                          "many GiB (achievable HBM bandwidth; byte-counter calibration)")
@@ -677,6 +680,7 @@ def main():
     import workloads as W
     from paper_2205_01848_amd import binding as B
 
+    B.moe_set_gemm_tiles(args.tiles)
     wl = W.config(args.workload)
     cap_rule = wl.capacity[-1]
     if args.capacity:
@@ -776,7 +780,8 @@ def main():
                    "E": wl.E, "k": wl.k, "d_ff": wl.f, "act": wl.act,
                    "capacity": f"{cap_rule[0]} {cap_rule[1]}/{cap_rule[2]}",
                    "rows": args.rows, "pass": "fwd+bwd" if wl.backward else "fwd",
-                   "row_align": L.row_align, "parallelism": "single GPU"},
+                   "row_align": L.row_align, "parallelism": "single GPU",
+                   "gemm_tiles": ["auto", "256x256", "128x128"][args.tiles]},
         "roofline": roof,
         "cpu_baseline": None,
         "detail": {"kept_rows": kept, "executed_rows": executed, "status": status,

@@ -72,13 +72,14 @@ SIGNATURES = {
     "moe_policy_end": (_c_int, [_p, _p, _p]),
     "moe_policy_state": (_c_int, [_p, _p, _p, _p, _p]),
     "moe_timing_enable": (_c_int, [_c_int]),
+    "moe_set_gemm_tiles": (_c_int, [_c_int]),
     "moe_timing_report": (_c_int, [ctypes.c_char_p, _c_size]),
 }
 
 _lib = None
 
 
-ABI_VERSION = 5   # moe_abi_version() of the library this binding is written for
+ABI_VERSION = 6   # moe_abi_version() of the library this binding is written for
 
 
 class MoEError(RuntimeError):
@@ -487,6 +488,11 @@ class CapacityPolicy:
 # ---- kernel timing (instrumentation) ----------------------------------------
 def moe_timing_enable(on: bool):
     _check(lib().moe_timing_enable(1 if on else 0), "moe_timing_enable")
+
+
+def moe_set_gemm_tiles(mode: int):
+    """0: automatic tile choice; 1: 256x256 tiles only; 2: 128x128 tiles only."""
+    _check(lib().moe_set_gemm_tiles(int(mode)), "moe_set_gemm_tiles")
 
 
 def moe_timing_report() -> dict:

@@ -45,6 +45,7 @@ constexpr int kStripBytes = kStripRows * kStripPitch * 4;
 constexpr int kStripsPerArray = kTileBytes / kStripBytes;
 static_assert(3 * kStripsPerArray >= 16, "two staging strips per wave in three operand buffers");
 
+constexpr int BM_S = 128;       // M tile of the two-workgroups-per-CU bf16 kernel
 constexpr int kGroupM = 4;      // M tiles per scheduling group
 constexpr int kXcds = 8;
 constexpr int kSplitFloor = 512;  // smallest K chunk of a split dW product
@@ -61,6 +62,7 @@ enum Act { ACT_RELU = 0, ACT_GELU = 1, ACT_SWIGLU = 2 };
 // Device-side schedule written by schedule_kernel.
 struct Sched {
   int n_mtiles;    // (expert, m0) tiles of BM rows
+  int n_mtiles_s;  // (expert, m0) tiles of BM_S rows (the 128x128-tile kernel)
   int n_segs;      // (expert, k range) segments of the dW products
   int kc;          // split chunk (rows)
   int n_slots;     // partial-sum slots used
@@ -169,8 +171,9 @@ __device__ __forceinline__ int64_t wave_incl_scan(int64_t v) {
 // in order and cuts the lists where the bounds stop them.
 __global__ __launch_bounds__(64) void schedule_kernel(
     const int32_t* __restrict__ offsets, const int32_t* __restrict__ rows, int E,
-    int64_t rows_alloc, int max_mtiles, int max_segs, int tmn_min, int max_slots,
-    Sched* __restrict__ s, int2* __restrict__ mtile, int4* __restrict__ seg) {
+    int64_t rows_alloc, int max_mtiles, int max_mtiles_s, int max_segs, int tmn_min,
+    int max_slots, Sched* __restrict__ s, int2* __restrict__ mtile, int2* __restrict__ mtile_s,
+    int4* __restrict__ seg) {
   const int g = threadIdx.x;
   // rows of expert g, clamped to its region and to rows_alloc
   int64_t m = 0;
@@ -185,6 +188,9 @@ __global__ __launch_bounds__(64) void schedule_kernel(
   const int64_t tiles = (m + BM - 1) / BM;
   const int64_t tiles_incl = wave_incl_scan(tiles);
   const int64_t tiles_total = __shfl(tiles_incl, 63, 64);
+  const int64_t tiles_s = (m + BM_S - 1) / BM_S;
+  const int64_t tiles_s_incl = wave_incl_scan(tiles_s);
+  const int64_t tiles_s_total = __shfl(tiles_s_incl, 63, 64);
   const int64_t kw = (m + kKc - 1) / kKc * kKc;
   const int64_t kwork = __shfl(wave_incl_scan(kw), 63, 64);
   int64_t kc = (kwork * tmn_min + 511) / 512;
@@ -196,13 +202,16 @@ __global__ __launch_bounds__(64) void schedule_kernel(
   // totals read from lane 63 while every lane is active
   const int64_t segs_total = __shfl(segs_incl, 63, 64);
   const int64_t slots_total = __shfl(slots_incl, 63, 64);
-  const bool fits = tiles_total <= max_mtiles && segs_total <= max_segs && slots_total <= max_slots;
+  const bool fits = tiles_total <= max_mtiles && tiles_s_total <= max_mtiles_s &&
+                    segs_total <= max_segs && slots_total <= max_slots;
   if (fits) {
     if (g < E) {
       const int mi = static_cast<int>(m);
       s->rows[g] = mi;
       const int t0 = static_cast<int>(tiles_incl - tiles);
       for (int i = 0; i < static_cast<int>(tiles); ++i) mtile[t0 + i] = make_int2(g, i * BM);
+      const int t0s = static_cast<int>(tiles_s_incl - tiles_s);
+      for (int i = 0; i < static_cast<int>(tiles_s); ++i) mtile_s[t0s + i] = make_int2(g, i * BM_S);
       const int n = static_cast<int>(nsp);
       const int s0 = static_cast<int>(segs_incl - nsp);
       const int q0 = static_cast<int>(slots_incl - (n > 1 ? n : 0));
@@ -216,6 +225,7 @@ __global__ __launch_bounds__(64) void schedule_kernel(
     }
     if (g == 0) {
       s->n_mtiles = static_cast<int>(tiles_total);
+      s->n_mtiles_s = static_cast<int>(tiles_s_total);
       s->n_segs = static_cast<int>(segs_total);
       s->n_slots = static_cast<int>(slots_total);
       s->kc = static_cast<int>(kc);
@@ -223,7 +233,7 @@ __global__ __launch_bounds__(64) void schedule_kernel(
     return;
   }
   if (g != 0) return;
-  int nm = 0;
+  int nm = 0, nms = 0;
   int64_t kwork_c = 0;
   for (int e = 0; e < E; ++e) {
     const int64_t off = offsets[e];
@@ -233,12 +243,15 @@ __global__ __launch_bounds__(64) void schedule_kernel(
     me = min(me, rows_alloc - off);
     me = max(me, int64_t(0));
     me = min(me, static_cast<int64_t>(max_mtiles - nm) * BM);
+    me = min(me, static_cast<int64_t>(max_mtiles_s - nms) * BM_S);
     const int mi = static_cast<int>(me);
     s->rows[e] = mi;
     for (int m0 = 0; m0 < mi; m0 += BM) mtile[nm++] = make_int2(e, m0);
+    for (int m0 = 0; m0 < mi; m0 += BM_S) mtile_s[nms++] = make_int2(e, m0);
     kwork_c += (mi + kKc - 1) / kKc * kKc;
   }
   s->n_mtiles = nm;
+  s->n_mtiles_s = nms;
   int64_t kcc = (kwork_c * tmn_min + 511) / 512;
   kcc = (kcc + kKc - 1) / kKc * kKc;
   kcc = max(kcc, static_cast<int64_t>(kSplitFloor));
@@ -922,8 +935,6 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_f32_kernel(const GemmPar
 // matrix core stays busy.  A 128x128 block reads a third less LDS per MFMA
 // than a 128x64 one.
 constexpr int kThreads16 = 256;
-constexpr int kP16 = 132;                      // floats per staged row (128 + 4)
-constexpr int kStrip16Bytes = 16 * kP16 * 4;   // 16 rows: two strips per 32 KB array
 
 typedef int intx4 __attribute__((ext_vector_type(4)));
 
@@ -1161,22 +1172,251 @@ __device__ __forceinline__ void mainloop16(const TileOps& op, char* la0, char* l
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 }
 
-// Stage rows 16i .. 16i+15 of the wave's accumulators as fp32, row pitch kP16.
-__device__ __forceinline__ void stage16(float* strip, const floatx4 (&acc)[8][8], int i,
+// ---------------------------------------------------------------------------
+// bf16 products on 128x128 tiles, two workgroups per CU
+// ---------------------------------------------------------------------------
+// The 256x256 kernel holds one wavefront per SIMD (256 accumulation
+// registers), so a tile's prologue and epilogue leave the matrix cores idle:
+// on short K (a few K steps per tile), few tiles per CU, or an epilogue heavy
+// in VALU work, that idle time is a large share.  This variant computes
+// 128x128 tiles with 4 wavefronts of 64x64 (64 accumulation registers,
+// under 256 registers in all) and 64 KB of LDS, so two workgroups share each
+// CU and one's epilogue overlaps the other's MFMAs.  It reads twice the
+// operand bytes per flop of the 256x256 tile, which is why large products
+// keep the big tile.  The K loop has the same structure: two stages of K 64,
+// two barriers per step, and loads and fragment reads issued one at a time
+// between the MFMAs.
+//
+// Wave w owns tile rows 64 (w >> 1) .. +63 and columns 64 (w & 1) .. +63
+// (gated forward: hidden units 32 (w & 1) .. +31 of W1, then the same units
+// of W3).  KC LDS tiles are 128 rows of 128 bytes with the swizzle of the
+// big tile; KM tiles are 64 k-rows of 128 elements (256 bytes) with the
+// same XOR of 32-element segments by k mod 4.
+template <int ALAY, int BLAY, bool GATED, bool FULL>
+__device__ __forceinline__ void mainloop16s(const TileOps& op, char* la0, char* lb0, char* la1,
+                                            char* lb1, floatx4 (&acc)[4][4], int zt) {
+  constexpr int KSTEP = 64;
+  constexpr int KMROW = 256;           // bytes per k-row of a KM tile
+  const int lane = (static_cast<int>(threadIdx.x) & 63) + zt;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int K = op.K;
+  const int nk = (K + KSTEP - 1) / KSTEP;
+  if (nk <= 0) return;
+  const int nk2 = (nk + 1) & ~1;   // odd counts load one all-zero step
+
+  // ---- loads: 1 KB blocks (8 rows of a KC tile: lane l -> row l >> 3,
+  // physical chunk l & 7; or 4 k-rows of a KM tile: lane l -> k-row l >> 4,
+  // physical elements 8 (l & 15) .. +7); wave w loads blocks 4w .. 4w+3 of
+  // A (g = 0..3) and of B (g = 4..7) of every stage.
+  const int l3 = lane >> 3;
+  const int co0 = ((lane & 7) ^ swz(l3)) * 16, co1 = ((lane & 7) ^ swz(l3 + 8)) * 16;
+  const int kr = lane >> 4;            // KM: k-row within the block (= k mod 4)
+  const int pe = (lane & 15) * 8;      // KM: physical element within the k-row
+  const int km_col = (((pe >> 5) ^ kr) << 5) + (pe & 31);
+  const __amdgpu_buffer_rsrc_t ra_t = tile_rsrc(op.a.base);
+  const __amdgpu_buffer_rsrc_t rb_t = tile_rsrc(op.b.base);
+  const __amdgpu_buffer_rsrc_t rb3_t = tile_rsrc(GATED ? op.b.base2 : op.b.base);
+  auto km_rsrc = [&](const Operand& o, int kt, bool second) {
+    const int64_t k = static_cast<int64_t>(kt) * KSTEP - (second ? o.split : 0);
+    return tile_rsrc((second ? o.base2 : o.base) + k * o.ld);
+  };
+  struct StepLd {
+    __amdgpu_buffer_rsrc_t ra, ra2, rb, rb2;
+    int kt;
+    bool kfull, kany;
+  };
+  auto step_ld = [&](int kt) {
+    StepLd s;
+    s.kt = kt;
+    s.kfull = (kt + 1) * KSTEP <= K;
+    s.kany = kt * KSTEP < K;
+    s.ra = ra_t; s.ra2 = ra_t; s.rb = rb_t; s.rb2 = rb3_t;
+    if constexpr (ALAY == L_KM) {
+      s.ra = km_rsrc(op.a, kt, false);
+      s.ra2 = op.a.base2 ? km_rsrc(op.a, kt, true) : s.ra;
+    }
+    if constexpr (BLAY == L_KM) {
+      s.rb = km_rsrc(op.b, kt, false);
+      s.rb2 = op.b.base2 ? km_rsrc(op.b, kt, true) : s.rb;
+    }
+    return s;
+  };
+  auto load_blk = [&](auto lay, const Operand& o, const __amdgpu_buffer_rsrc_t& rs,
+                      const __amdgpu_buffer_rsrc_t& rs2, char* dst, int blk, const StepLd& s,
+                      bool gated) {
+    constexpr int LAY = decltype(lay)::value;
+    const int ld = static_cast<int>(o.ld);
+    uint32_t off;
+    int soff;
+    bool second = false;
+    if constexpr (LAY == L_KC) {
+      const int co = (blk & 1) ? co1 : co0;
+      // gated forward: 32-row groups alternate W1 / W3 rows of 32 hidden units
+      const int row0 = gated ? (blk >> 3) * 32 + (blk & 3) * 8 : blk * 8;
+      second = gated && ((blk >> 2) & 1);
+      off = static_cast<uint32_t>(l3 * ld) + co;
+      soff = row0 * ld + s.kt * kRowBytes;
+      if (!FULL || !s.kfull) {
+        const bool ok = (FULL || row0 + l3 < o.rows) && (s.kfull || s.kt * kRowBytes + co < K * 2);
+        if (!ok) off = kOob;
+      }
+    } else {
+      const int krel = 4 * blk;                  // first k-row of the block in the step
+      const int kabs = s.kt * KSTEP + krel;
+      second = kabs >= o.split;                  // split is a multiple of 8: no block straddles it
+      off = static_cast<uint32_t>(kr * ld + km_col * 2);
+      soff = krel * ld;
+      if (!FULL || !s.kfull) {
+        const bool ok = (FULL || km_col < o.rows) && (s.kfull || kabs + kr < K);
+        if (!ok) off = kOob;
+      }
+    }
+    if (!s.kany) off = kOob;
+    if (second)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs2, MOE_LDS(dst + blk * 1024), 16, off, soff, 0, 0);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, MOE_LDS(dst + blk * 1024), 16, off, soff, 0, 0);
+  };
+  using KC_ = std::integral_constant<int, L_KC>;
+  using KM_ = std::integral_constant<int, L_KM>;
+  auto load1 = [&](const StepLd& s, char* sa, char* sb, int g) {
+    const int blk = wave * 4 + (g & 3);
+    if (g < 4) {
+      if constexpr (ALAY == L_KC) load_blk(KC_{}, op.a, s.ra, s.ra2, sa, blk, s, false);
+      else load_blk(KM_{}, op.a, s.ra, s.ra2, sa, blk, s, false);
+    } else {
+      if constexpr (BLAY == L_KC) load_blk(KC_{}, op.b, s.rb, s.rb2, sb, blk, s, GATED);
+      else load_blk(KM_{}, op.b, s.rb, s.rb2, sb, blk, s, false);
+    }
+  };
+
+  // ---- fragments (as in the 256x256 kernel; KM k-rows are 256 bytes)
+  const int c16 = lane & 15, G = lane >> 4;
+  const int fa_kc = (wm * 64 + c16) * kRowBytes, fb_kc = (wn * 64 + c16) * kRowBytes;
+  auto km_frag = [&](const char* st, int cb, int h) -> uint4 {
+    const int phys = (((cb >> 5) ^ (c16 >> 2)) << 5) + (cb & 31) + 4 * (c16 & 3);
+    const char* p0 = st + (32 * h + 8 * G + (c16 >> 2)) * KMROW + phys * 2;
+    const uint2 lo = read_tr(p0);
+    const uint2 hi = read_tr(p0 + 4 * KMROW);
+    return make_uint4(lo.x, lo.y, hi.x, hi.y);
+  };
+  // fragment g of half h: A sub-block g (g < 4) or B sub-block g - 4
+  auto read1 = [&](const char* sa, const char* sb, int h, uint4 (&fa)[4], uint4 (&fb)[4], int g) {
+    const int sw = ((4 * h + G) ^ (c16 >> 1)) << 4;
+    if (g < 4) {
+      if constexpr (ALAY == L_KC)
+        fa[g] = *reinterpret_cast<const uint4*>(sa + fa_kc + g * 16 * kRowBytes + sw);
+      else
+        fa[g] = km_frag(sa, wm * 64 + g * 16, h);
+    } else {
+      if constexpr (BLAY == L_KC)
+        fb[g - 4] = *reinterpret_cast<const uint4*>(sb + fb_kc + (g - 4) * 16 * kRowBytes + sw);
+      else
+        fb[g - 4] = km_frag(sb, wn * 64 + (g - 4) * 16, h);
+    }
+  };
+  uint4 f0a[4], f0b[4], f1a[4], f1b[4];
+
+  // One K step from stage (ca, cb), the next stage in (na, nb); the loads of
+  // step kt + 2 go into (ca, cb).  MFMAs in groups of two (m -> block
+  // m >> 2, m & 3); the first quarter reads the A fragments of k-half 1, the
+  // second the B fragments and issues the A loads, the second half reads the
+  // next stage's k-half 0 and issues the B loads.
+  auto step = [&](int kt, char* ca, char* cb, const char* na, const char* nb) {
+    const StepLd s = step_ld(kt + 2);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      read1(ca, cb, 1, f1a, f1b, g);
+#pragma unroll
+      for (int m = 2 * g; m < 2 * g + 2; ++m) mfma16(acc[m >> 2][m & 3], f0a[m >> 2], f0b[m & 3]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int g = 4; g < 8; ++g) {
+      load1(s, ca, cb, g - 4);
+      read1(ca, cb, 1, f1a, f1b, g);
+#pragma unroll
+      for (int m = 2 * g; m < 2 * g + 2; ++m) mfma16(acc[m >> 2][m & 3], f0a[m >> 2], f0b[m & 3]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // stage kt + 1 has landed (only the 4 A loads just issued may be pending)
+    __builtin_amdgcn_s_waitcnt(0x0074);   // vmcnt(4) lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      if ((g & 1) == 0) load1(s, ca, cb, 4 + (g >> 1));
+      read1(na, nb, 0, f0a, f0b, g);
+#pragma unroll
+      for (int m = 2 * g; m < 2 * g + 2; ++m) mfma16(acc[m >> 2][m & 3], f1a[m >> 2], f1b[m & 3]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  {
+    const StepLd s0 = step_ld(0), s1 = step_ld(1);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) load1(s0, la0, lb0, g);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) load1(s1, la1, lb1, g);
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F78);   // vmcnt(8): this wave's stage-0 loads landed
+  __builtin_amdgcn_s_barrier();
+#pragma unroll
+  for (int g = 0; g < 8; ++g) read1(la0, lb0, 0, f0a, f0b, g);
+  for (int kt = 0; kt < nk2; kt += 2) {
+    step(kt, la0, lb0, la1, lb1);
+    step(kt + 1, la1, lb1, la0, lb0);
+  }
+  __builtin_amdgcn_s_waitcnt(0x0070);
+  __builtin_amdgcn_s_barrier();   // every load landed, every read done: stages are free
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
+
+// Wave-block shapes of the two bf16 kernels: RB x CB blocks of 16x16 per
+// wave, 2 x 2 waves per workgroup.
+template <int RB_, int CB_, int MINB_> struct Tile16 {
+  static constexpr int RB = RB_, CB = CB_;
+  static constexpr int WR = 16 * RB, WC = 16 * CB;      // wave block
+  static constexpr int TM = 2 * WR, TN = 2 * WC;        // workgroup tile
+  static constexpr int kP = WC + 4;                     // strip pitch (floats): rows 4 apart
+                                                        // fall 16 banks apart
+  static constexpr int kStripBytes = 16 * kP * 4;
+  static constexpr int kStageBytes = TM * kRowBytes;    // one operand of one stage
+  static constexpr int kMinBlocks = MINB_;              // workgroups per CU
+  static_assert(2 * kStripBytes <= kStageBytes, "two staging strips per operand buffer");
+};
+using TileBig = Tile16<8, 8, 1>;
+using TileSmall = Tile16<4, 4, 2>;
+static_assert(TileBig::TM == BM && TileBig::TN == BN && TileSmall::TM == BM_S, "tile sizes");
+
+// Stage rows 16i .. 16i+15 of the wave's accumulators as fp32, row pitch C::kP.
+template <typename C>
+__device__ __forceinline__ void stage16(float* strip, const floatx4 (&acc)[C::RB][C::CB], int i,
                                         int lane) {
   const int c16 = lane & 15, G = lane >> 4;
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
+  for (int j = 0; j < C::CB; ++j)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) strip[(4 * G + q) * kP16 + 16 * j + c16] = acc[i][j][q];
+    for (int q = 0; q < 4; ++q) strip[(4 * G + q) * C::kP + 16 * j + c16] = acc[i][j][q];
 }
 
-template <int MODE, int PASS>
-__global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmParams p) {
-  __shared__ __attribute__((aligned(16))) char la0[kTileBytes];
-  __shared__ __attribute__((aligned(16))) char lb0[kTileBytes];
-  __shared__ __attribute__((aligned(16))) char la1[kTileBytes];
-  __shared__ __attribute__((aligned(16))) char lb1[kTileBytes];
+template <int MODE, int PASS, typename C>
+__global__ __launch_bounds__(kThreads16, C::kMinBlocks) void ffn_gemm16_kernel(const GemmParams p) {
+  __shared__ __attribute__((aligned(16))) char la0[C::kStageBytes];
+  __shared__ __attribute__((aligned(16))) char lb0[C::kStageBytes];
+  __shared__ __attribute__((aligned(16))) char la1[C::kStageBytes];
+  __shared__ __attribute__((aligned(16))) char lb1[C::kStageBytes];
+  constexpr bool SMALL = C::RB == 4;
+  constexpr int TM = C::TM, TN = C::TN, WR = C::WR, WC = C::WC, kP = C::kP;
   using T = uint16_t;
   constexpr int ES = 2;
   constexpr bool VARK = MODE == M_DW;
@@ -1186,7 +1426,8 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const Sched& sc = *p.sched;
-  const int n_items = VARK ? sc.n_segs * p.mtiles_out * p.ntiles : sc.n_mtiles * p.ntiles;
+  const int n_mt = SMALL ? sc.n_mtiles_s : sc.n_mtiles;
+  const int n_items = VARK ? sc.n_segs * p.mtiles_out * p.ntiles : n_mt * p.ntiles;
   const int G = gridDim.x;
   const int lbase = (blockIdx.x % kXcds) * (G / kXcds) + blockIdx.x / kXcds;
 
@@ -1198,28 +1439,28 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
     int slot = -1, mt, nt;
     if constexpr (!VARK) {
       int mti;
-      decode_banded(L, sc.n_mtiles, p.ntiles, mti, nt);
+      decode_banded(L, n_mt, p.ntiles, mti, nt);
       const int2 tm = p.mtile[mti];
       g = tm.x;
       row0 = p.offsets[g] + tm.y;
-      m_valid = min(BM, sc.rows[g] - tm.y);
+      m_valid = min(TM, sc.rows[g] - tm.y);
       op.a = {p.A + static_cast<int64_t>(row0) * p.lda, nullptr, p.lda, m_valid, 0};
       op.K = p.K;
       const char* bg = p.B + static_cast<int64_t>(g) * p.b_gstride;
       if constexpr (GATED) {
-        n0 = nt * (BN / 2);
+        n0 = nt * (TN / 2);
         op.b = {bg + static_cast<int64_t>(n0) * p.ldb,
                 p.B2 + static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0) * p.ldb,
-                p.ldb, min(BN / 2, p.N - n0), 0};
+                p.ldb, min(TN / 2, p.N - n0), 0};
       } else if constexpr (BLAY == L_KC) {
-        n0 = nt * BN;
-        op.b = {bg + static_cast<int64_t>(n0) * p.ldb, nullptr, p.ldb, min(BN, p.N - n0), 0};
+        n0 = nt * TN;
+        op.b = {bg + static_cast<int64_t>(n0) * p.ldb, nullptr, p.ldb, min(TN, p.N - n0), 0};
       } else {
-        n0 = nt * BN;
+        n0 = nt * TN;
         op.b = {bg + static_cast<int64_t>(n0) * ES,
                 p.B2 ? p.B2 + static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0) * ES
                      : nullptr,
-                p.ldb, min(BN, p.N - n0), p.B2 ? p.kmsplit : 0x7FFFFFFF};
+                p.ldb, min(TN, p.N - n0), p.B2 ? p.kmsplit : 0x7FFFFFFF};
       }
     } else {
       const int tmn = p.mtiles_out * p.ntiles;
@@ -1230,13 +1471,13 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
       slot = sg.w;
       const int k1 = min(sg.z, sc.rows[g]);
       const int64_t krow = static_cast<int64_t>(p.offsets[g]) + sg.y;
-      row0 = mt * BM;
-      n0 = nt * BN;
-      m_valid = min(BM, p.M_out - row0);
+      row0 = mt * TM;
+      n0 = nt * TN;
+      m_valid = min(TM, p.M_out - row0);
       op.a = {p.A + krow * p.lda + static_cast<int64_t>(row0) * ES, nullptr, p.lda, m_valid,
               0x7FFFFFFF};
       op.b = {p.B + krow * p.ldb + static_cast<int64_t>(n0) * ES, nullptr, p.ldb,
-              min(BN, p.N - n0), 0x7FFFFFFF};
+              min(TN, p.N - n0), 0x7FFFFFFF};
       op.K = max(0, k1 - sg.y);
     }
 
@@ -1245,11 +1486,15 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
     // of the tile loop and spilled (their reloads would wait on the loads)
     int zt;
     asm volatile("s_mov_b32 %0, 0" : "=s"(zt));
-    floatx4 acc[8][8];
-    if (op.a.rows >= BM && op.b.rows >= (GATED ? BN / 2 : BN))
-      mainloop16<ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc, zt);
-    else
-      mainloop16<ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc, zt);
+    floatx4 acc[C::RB][C::CB];
+    const bool full = op.a.rows >= TM && op.b.rows >= (GATED ? TN / 2 : TN);
+    if constexpr (SMALL) {
+      if (full) mainloop16s<ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc, zt);
+      else mainloop16s<ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc, zt);
+    } else {
+      if (full) mainloop16<ALAY, BLAY, GATED, true>(op, la0, lb0, la1, lb1, acc, zt);
+      else mainloop16<ALAY, BLAY, GATED, false>(op, la0, lb0, la1, lb1, acc, zt);
+    }
 
     // Epilogue, wave by wave: 16 accumulator rows at a time go through the
     // wave's LDS strip; a lane then finishes 8 consecutive columns of a row
@@ -1260,28 +1505,61 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
     int z;
     asm volatile("s_mov_b32 %0, 0" : "=s"(z));
     const int el = lane + z;
-    float* strip = reinterpret_cast<float*>((wave < 2 ? la0 : lb0) + (wave & 1) * kStrip16Bytes + z);
-    const int wr0 = wm * 128;                     // the wave's first tile row
+    float* strip = reinterpret_cast<float*>((wave < 2 ? la0 : lb0) + (wave & 1) * C::kStripBytes + z);
+    const int wr0 = wm * WR;                      // the wave's first tile row
+    // weight gradients: where the fp32 result of tile row orow, column gc goes
+    // (a split partial-sum slot, or the first or second gradient array)
+    auto dw_dst = [&](int orow, int gc) -> float* {
+      if (slot >= 0)
+        return p.partial + static_cast<int64_t>(slot) * p.slot_elems +
+               static_cast<int64_t>(orow) * p.N + gc;
+      if (orow < p.split_row)
+        return p.dwA + static_cast<int64_t>(g) * p.dw_gstride + static_cast<int64_t>(orow) * p.N + gc;
+      return p.dwB + static_cast<int64_t>(g) * p.dw_gstride +
+             static_cast<int64_t>(orow - p.split_row) * p.N + gc;
+    };
+    if constexpr (VARK) {
+      if (op.K == 0) {
+        // no rows to contract over (an expert without rows): the tile is
+        // zero; each lane stores 8 zeros per row pass straight to memory,
+        // with no staging, so the tile costs only its stores.  Every wave
+        // of the workgroup takes this path, and none touched the LDS.
+        constexpr int LR = WC / 8, RG = 64 / LR;
+        const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+        for (int r = 0; r < WR; r += RG) {
+          const int lm = wr0 + r + el / LR, gc = n0 + wn * WC + (el % LR) * 8;
+          if (lm < m_valid && gc < p.N) {
+            float* dst = dw_dst(row0 + lm, gc);
+            *reinterpret_cast<float4*>(dst) = zero;
+            *reinterpret_cast<float4*>(dst + 4) = zero;
+          }
+        }
+        continue;
+      }
+    }
     // ReLU / GELU layers: the epilogue is specialised on the activation, one
     // uniform branch per tile instead of one per element
     auto epilogue = [&](auto act_c) {
     constexpr int ACT = decltype(act_c)::value;
     if constexpr (MODE == M_FWD1_SWIGLU) {
-      // strip columns [0,64): H1, [64,128): H3 of hidden units n0 + 64 wn + u
+      // strip columns [0,U): H1, [U,2U): H3 of hidden units n0 + U wn + u, U =
+      // WC / 2; LU lanes cover a row's U units, 8 each
+      constexpr int U = WC / 2, LU = U / 8, RU = 64 / LU;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        stage16(strip, acc, i, el);
+      for (int i = 0; i < C::RB; ++i) {
+        stage16<C>(strip, acc, i, el);
 #pragma unroll
-        for (int it = 0; it < 2; ++it) {
-          const int r = it * 8 + (el >> 3), u8 = (el & 7) * 8;
+        for (int it = 0; it < 16 / RU; ++it) {
+          const int r = it * RU + el / LU, u8 = (el % LU) * 8;
           const int lm = wr0 + 16 * i + r;
-          const int gc = n0 + wn * 64 + u8;
+          const int gc = n0 + wn * U + u8;
           if (lm < m_valid && gc < p.N) {
             float h1[8], h3[8], a[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-              h1[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kP16 + u8 + e]));
-              h3[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kP16 + 64 + u8 + e]));
+              h1[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kP + u8 + e]));
+              h3[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kP + U + u8 + e]));
               a[e] = h1[e] * sigm(h1[e]) * h3[e];
             }
             const int64_t grow = row0 + lm;
@@ -1294,15 +1572,18 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
         }
       }
     } else if constexpr (MODE == M_BWD_DA || MODE == M_BWD_DA_SWIGLU) {
-      // dH = dA act'(H): 32 (row block, row group) iterations, each reading 8
+      // dH = dA act'(H): (row block, row group) iterations, each reading 8
       // saved pre-activations (two planes for SwiGLU) per lane, issued kPf
-      // iterations ahead of their use into a ring of kPf + 1 registers
+      // iterations ahead of their use into a ring of kPf + 1 registers.  LR
+      // lanes cover a row of the wave block, RG rows form a group, GB groups
+      // a 16-row block.
       constexpr bool SW = MODE == M_BWD_DA_SWIGLU;
-      constexpr int kIt = 32, kPf = 4, kRing = kPf + 1;
+      constexpr int LR = WC / 8, RG = 64 / LR, GB = 16 / RG;
+      constexpr int kIt = C::RB * GB, kPf = 4, kRing = kPf + 1;
       Raw8<T> q1[kRing], q3[kRing];
       auto pos = [&](int n, int& lm, int& gc) {
-        lm = wr0 + 16 * (n >> 2) + 4 * (n & 3) + (el >> 4);
-        gc = n0 + wn * 128 + (el & 15) * 8;
+        lm = wr0 + 16 * (n / GB) + RG * (n % GB) + el / LR;
+        gc = n0 + wn * WC + (el % LR) * 8;
       };
       auto issue = [&](int n) {
         int lm, gc;
@@ -1319,11 +1600,11 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
 #pragma unroll
       for (int n = 0; n < kIt; ++n) {
         if (n + kPf < kIt) issue(n + kPf);
-        if ((n & 3) == 0) stage16(strip, acc, n >> 2, el);
+        if (n % GB == 0) stage16<C>(strip, acc, n / GB, el);
         int lm, gc;
         pos(n, lm, gc);
         if (lm < m_valid && gc < p.N) {
-          const int r = 4 * (n & 3) + (el >> 4), c8 = (el & 15) * 8;
+          const int r = RG * (n % GB) + el / LR, c8 = (el % LR) * 8;
           const int64_t grow = row0 + lm;
           float h1[8], g1[8];
           q1[n % kRing].to_f(h1);
@@ -1332,7 +1613,7 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
             q3[n % kRing].to_f(h3);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-              const float da = strip[r * kP16 + c8 + e];
+              const float da = strip[r * kP + c8 + e];
               const float sg = sigm(h1[e]);
               g1[e] = da * h3[e] * sg * (1.f + h1[e] * (1.f - sg));
               g3[e] = da * h1[e] * sg;
@@ -1342,35 +1623,25 @@ __global__ __launch_bounds__(kThreads16, 1) void ffn_gemm16_kernel(const GemmPar
           } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-              g1[e] = strip[r * kP16 + c8 + e] * act_grad_f(h1[e], ACT);
+              g1[e] = strip[r * kP + c8 + e] * act_grad_f(h1[e], ACT);
             store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
           }
         }
       }
     } else {
+      constexpr int LR = WC / 8, RG = 64 / LR;   // lanes per row, rows per pass
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        stage16(strip, acc, i, el);
+      for (int i = 0; i < C::RB; ++i) {
+        stage16<C>(strip, acc, i, el);
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-          const int r = 4 * it + (el >> 4), c8 = (el & 15) * 8;
+        for (int it = 0; it < 16 / RG; ++it) {
+          const int r = RG * it + el / LR, c8 = (el % LR) * 8;
           const int lm = wr0 + 16 * i + r;
-          const int gc = n0 + wn * 128 + c8;
+          const int gc = n0 + wn * WC + c8;
           if (lm < m_valid && gc < p.N) {
-            const float* sp = strip + r * kP16 + c8;
+            const float* sp = strip + r * kP + c8;
             if constexpr (MODE == M_DW) {
-              const int orow = row0 + lm;
-              float* dst;
-              if (slot >= 0) {
-                dst = p.partial + static_cast<int64_t>(slot) * p.slot_elems +
-                      static_cast<int64_t>(orow) * p.N + gc;
-              } else if (orow < p.split_row) {
-                dst = p.dwA + static_cast<int64_t>(g) * p.dw_gstride +
-                      static_cast<int64_t>(orow) * p.N + gc;
-              } else {
-                dst = p.dwB + static_cast<int64_t>(g) * p.dw_gstride +
-                      static_cast<int64_t>(orow - p.split_row) * p.N + gc;
-              }
+              float* dst = dw_dst(row0 + lm, gc);
               *reinterpret_cast<float4*>(dst) = make_float4(sp[0], sp[1], sp[2], sp[3]);
               *reinterpret_cast<float4*>(dst + 4) = make_float4(sp[4], sp[5], sp[6], sp[7]);
             } else {
@@ -1473,10 +1744,10 @@ struct FfnPlan {
   int E, d, f, F;            // F = f (relu/gelu) or 2f (swiglu)
   int64_t rows_alloc;
   size_t es;
-  int max_mtiles, max_segs, max_slots, tmn_min;
+  int max_mtiles, max_mtiles_s, max_segs, max_slots, tmn_min;
   int64_t slot_elems;
   // byte offsets inside the workspace
-  size_t o_sched, o_mtile, o_seg, o_end_sched;
+  size_t o_sched, o_mtile, o_mtile_s, o_seg, o_end_sched;
   size_t o_abuf, o_dh, o_part, total_fwd, total_bwd;
 };
 
@@ -1493,6 +1764,7 @@ bool make_plan(moe_dtype dt, moe_act act, int E, int d, int f, int64_t rows_allo
   const int64_t max_ld = static_cast<int64_t>(pl.es) * (2 * static_cast<int64_t>(f) > d ? 2 * static_cast<int64_t>(f) : d);
   if (max_ld > kMaxOperandRowBytes) return false;
   pl.max_mtiles = cdiv(rows_alloc, BM) + E;
+  pl.max_mtiles_s = cdiv(rows_alloc, BM_S) + E;
   const int tmn2 = cdiv(d, BM) * cdiv(f, BN);
   const int tmn13 = cdiv(pl.F, BM) * cdiv(d, BN);
   pl.tmn_min = tmn2 < tmn13 ? tmn2 : tmn13;
@@ -1506,6 +1778,7 @@ bool make_plan(moe_dtype dt, moe_act act, int E, int d, int f, int64_t rows_allo
   size_t o = 0;
   pl.o_sched = o; o = align_up(o + sizeof(Sched), 256);
   pl.o_mtile = o; o = align_up(o + sizeof(int2) * pl.max_mtiles, 256);
+  pl.o_mtile_s = o; o = align_up(o + sizeof(int2) * pl.max_mtiles_s, 256);
   pl.o_seg = o;   o = align_up(o + sizeof(int4) * pl.max_segs, 256);
   pl.o_end_sched = o;
   const size_t es = pl.es;
@@ -1524,8 +1797,9 @@ moe_status launch_schedule(hipStream_t s, const FfnPlan& pl, const int32_t* offs
                            const int32_t* rows, char* ws) {
   MOE_TIMED("ffn_schedule", s);
   schedule_kernel<<<1, 64, 0, s>>>(
-      offsets, rows, pl.E, pl.rows_alloc, pl.max_mtiles, pl.max_segs, pl.tmn_min, pl.max_slots,
-      reinterpret_cast<Sched*>(ws + pl.o_sched), reinterpret_cast<int2*>(ws + pl.o_mtile),
+      offsets, rows, pl.E, pl.rows_alloc, pl.max_mtiles, pl.max_mtiles_s, pl.max_segs, pl.tmn_min,
+      pl.max_slots, reinterpret_cast<Sched*>(ws + pl.o_sched),
+      reinterpret_cast<int2*>(ws + pl.o_mtile), reinterpret_cast<int2*>(ws + pl.o_mtile_s),
       reinterpret_cast<int4*>(ws + pl.o_seg));
   MOE_LAUNCH_CHECK();
   return MOE_OK;
@@ -1541,20 +1815,59 @@ GemmParams base_params(const FfnPlan& pl, const int32_t* offsets, char* ws) {
   return p;
 }
 
+// Tile choice of the bf16 products (moe_set_gemm_tiles: 0 automatic, 1 the
+// 256x256 kernel only, 2 the 128x128 kernel only).
+int g_tile_mode = 0;
+
+// The 128x128 kernel runs two workgroups per CU, so one's prologue and
+// epilogue overlap the other's MFMAs, but it reads twice the operand bytes
+// per flop: on products that fill every CU for many rounds it takes about
+// 1.3 times as long per flop as the 256x256 kernel.  It pays off where the
+// 256x256 tiles leave CUs idle, mostly in the last round.  The host knows
+// N, K and the row budget, not the per-expert rows, so it estimates both
+// kernels' tile counts as if each expert held rows_alloc / E rows, counts
+// the rounds of the persistent grids (one 256x256 tile or two 128x128
+// tiles per CU at a time), and takes the 128x128 kernel when its rounds,
+// each worth about 0.65 of a 256x256 round, take less time.
+bool use_small_tiles(const FfnPlan& pl, moe_dtype dt, bool vark, bool gated, int N, int M_out) {
+  if (dt != MOE_BF16) return false;
+  if (g_tile_mode == 1) return false;
+  if (g_tile_mode == 2) return true;
+  const int64_t per = cdiv(pl.rows_alloc, pl.E);
+  auto tiles = [&](int tm, int tn) -> int64_t {
+    const int64_t nt = cdiv(N, gated ? tn / 2 : tn);
+    return vark ? static_cast<int64_t>(pl.E) * cdiv(M_out, tm) * nt
+                : static_cast<int64_t>(pl.E) * cdiv(per, tm) * nt;
+  };
+  const int64_t G = persistent_grid();
+  const int64_t rounds_big = (tiles(BM, BN) + G - 1) / G;
+  const int64_t rounds_small = (tiles(BM_S, BM_S) + 2 * G - 1) / (2 * G);
+  return 13 * rounds_small < 20 * rounds_big;
+}
+
 const char* pass_name(int pass) {
   static const char* names[] = {"gemm_fwd_h", "gemm_fwd_y", "gemm_bwd_da", "gemm_bwd_dx",
                                 "gemm_bwd_dw2", "gemm_bwd_dw13"};
   return names[pass];
 }
 
+// Launches one product; sets the tile counts along N (and M for the weight
+// gradients) for the kernel it picks.
 template <int MODE, int PASS>
-moe_status launch_gemm(hipStream_t s, moe_dtype dt, const GemmParams& p) {
-  const int grid = persistent_grid();
+moe_status launch_gemm(hipStream_t s, moe_dtype dt, const FfnPlan& pl, char* ws, GemmParams p) {
+  constexpr bool VARK = MODE == M_DW, GATED = MODE == M_FWD1_SWIGLU;
+  const bool small = use_small_tiles(pl, dt, VARK, GATED, p.N, p.M_out);
+  const int tm = small ? BM_S : BM, tn = small ? BM_S : BN;
+  p.ntiles = cdiv(p.N, GATED ? tn / 2 : tn);
+  if (VARK) p.mtiles_out = cdiv(p.M_out, tm);
+  if (small) p.mtile = reinterpret_cast<const int2*>(ws + pl.o_mtile_s);
   MOE_TIMED(pass_name(PASS), s);
-  if (dt == MOE_BF16)
-    ffn_gemm16_kernel<MODE, PASS><<<grid, kThreads16, 0, s>>>(p);
+  if (dt == MOE_BF16 && small)
+    ffn_gemm16_kernel<MODE, PASS, TileSmall><<<2 * persistent_grid(), kThreads16, 0, s>>>(p);
+  else if (dt == MOE_BF16)
+    ffn_gemm16_kernel<MODE, PASS, TileBig><<<persistent_grid(), kThreads16, 0, s>>>(p);
   else
-    ffn_gemm_f32_kernel<MODE, PASS><<<grid, kThreads, 0, s>>>(p);
+    ffn_gemm_f32_kernel<MODE, PASS><<<persistent_grid(), kThreads, 0, s>>>(p);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }
@@ -1565,16 +1878,18 @@ moe_status launch_gemm(hipStream_t s, moe_dtype dt, const GemmParams& p) {
     if (st_ != MOE_OK) return st_;         \
   } while (0)
 
+// dW[g] = sum of expert g's split slots: rows [0, split_row) of the [M_out, N]
+// result go to dwA, the rest to dwB; dw_gstride is the per-expert stride of
+// dwA and dwB (f x d for [dW1; dW3], whose M_out is 2f under SwiGLU).
 moe_status launch_split_reduce(hipStream_t s, const FfnPlan& pl, char* ws, int M_out, int N,
-                               float* dwA, float* dwB, int split_row) {
+                               float* dwA, float* dwB, int split_row, int64_t dw_gstride) {
   const int64_t elems = static_cast<int64_t>(M_out) * N;
   const int64_t bx = cdiv(elems, 1024);
   dim3 grid(static_cast<unsigned>(bx < kReduceBlocks ? bx : kReduceBlocks), pl.E);
   MOE_TIMED("split_reduce", s);
   split_reduce_kernel<<<grid, 256, 0, s>>>(
       reinterpret_cast<const float*>(ws + pl.o_part), elems,
-      reinterpret_cast<const Sched*>(ws + pl.o_sched), dwA, dwB, static_cast<int64_t>(M_out) * N,
-      split_row, N);
+      reinterpret_cast<const Sched*>(ws + pl.o_sched), dwA, dwB, dw_gstride, split_row, N);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }
@@ -1583,6 +1898,12 @@ moe_status launch_split_reduce(hipStream_t s, const FfnPlan& pl, char* ws, int M
 }  // namespace moe
 
 using namespace moe;
+
+extern "C" moe_status moe_set_gemm_tiles(int mode) {
+  if (mode < 0 || mode > 2) return MOE_EINVAL;
+  g_tile_mode = mode;
+  return MOE_OK;
+}
 
 extern "C" size_t moe_ffn_fwd_workspace_bytes(moe_dtype dt, moe_act act, int E, int d, int f,
                                               int64_t rows_alloc) {
@@ -1638,13 +1959,8 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   p.H1 = h_planes > 0 ? static_cast<char*>(h_save) : nullptr;
   p.H3 = h_save && sw ? static_cast<char*>(h_save) + plane : nullptr;
   p.ldh = f * es;
-  if (sw) {
-    p.ntiles = cdiv(f, BN / 2);
-    MOE_TRY(launch_gemm<M_FWD1_SWIGLU, P_FWD_H>(s, dt, p));
-  } else {
-    p.ntiles = cdiv(f, BN);
-    MOE_TRY(launch_gemm<M_FWD1, P_FWD_H>(s, dt, p));
-  }
+  if (sw) MOE_TRY(launch_gemm<M_FWD1_SWIGLU, P_FWD_H>(s, dt, pl, ws, p));
+  else MOE_TRY(launch_gemm<M_FWD1, P_FWD_H>(s, dt, pl, ws, p));
 
   GemmParams q = base_params(pl, offsets, ws);
   q.A = abuf;
@@ -1654,10 +1970,9 @@ extern "C" moe_status moe_expert_ffn_fwd(void* stream, moe_dtype dt, moe_act act
   q.b_gstride = static_cast<int64_t>(d) * f * es;
   q.K = f;
   q.N = d;
-  q.ntiles = cdiv(d, BN);
   q.C = static_cast<char*>(y_disp);
   q.ldc = d * es;
-  MOE_TRY(launch_gemm<M_STORE, P_FWD_Y>(s, dt, q));
+  MOE_TRY(launch_gemm<M_STORE, P_FWD_Y>(s, dt, pl, ws, q));
   return MOE_OK;
 }
 
@@ -1706,10 +2021,9 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
     q.b_gstride = static_cast<int64_t>(f) * d * es;
     q.K = F;
     q.N = d;
-    q.ntiles = cdiv(d, BN);
     q.C = static_cast<char*>(dx_disp);
     q.ldc = d * es;
-    return launch_gemm<M_STORE, P_BWD_DX>(s, dt, q);
+    return launch_gemm<M_STORE, P_BWD_DX>(s, dt, pl, ws, q);
   };
   // Order of the four products: dA first (it writes dH), dX right after it,
   // except when dx_disp is small enough to stay in the last-level cache: then
@@ -1726,7 +2040,6 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   p.b_gstride = static_cast<int64_t>(d) * f * es;
   p.K = d;
   p.N = f;
-  p.ntiles = cdiv(f, BN);
   p.act = actc;
   p.C = dh;
   p.ldc = F * es;
@@ -1734,8 +2047,8 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   p.H3 = const_cast<char*>(h3);
   p.ldh = f * es;
   p.f = f;
-  if (sw) MOE_TRY(launch_gemm<M_BWD_DA_SWIGLU, P_BWD_DA>(s, dt, p));
-  else MOE_TRY(launch_gemm<M_BWD_DA, P_BWD_DA>(s, dt, p));
+  if (sw) MOE_TRY(launch_gemm<M_BWD_DA_SWIGLU, P_BWD_DA>(s, dt, pl, ws, p));
+  else MOE_TRY(launch_gemm<M_BWD_DA, P_BWD_DA>(s, dt, pl, ws, p));
   if (!dx_last) MOE_TRY(launch_dx());
 
   // dW2 [d, f] = dY^T A, contracting over each expert's dispatched rows
@@ -1743,38 +2056,34 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   r.A = static_cast<const char*>(dy_disp);
   r.lda = d * es;
   r.M_out = d;
-  r.mtiles_out = cdiv(d, BM);
   r.B = abuf;
   r.ldb = f * es;
   r.N = f;
-  r.ntiles = cdiv(f, BN);
   r.dwA = dw2;
   r.dwB = dw2;
   r.dw_gstride = static_cast<int64_t>(d) * f;
   r.split_row = d;
   r.partial = reinterpret_cast<float*>(ws + pl.o_part);
   r.slot_elems = static_cast<int64_t>(d) * f;
-  MOE_TRY(launch_gemm<M_DW, P_BWD_DW2>(s, dt, r));
-  MOE_TRY(launch_split_reduce(s, pl, ws, d, f, dw2, dw2, d));
+  MOE_TRY(launch_gemm<M_DW, P_BWD_DW2>(s, dt, pl, ws, r));
+  MOE_TRY(launch_split_reduce(s, pl, ws, d, f, dw2, dw2, d, r.dw_gstride));
 
   // [dW1; dW3] [F, d] = [dH1 dH3]^T X
   GemmParams u = base_params(pl, offsets, ws);
   u.A = dh;
   u.lda = F * es;
   u.M_out = F;
-  u.mtiles_out = cdiv(F, BM);
   u.B = static_cast<const char*>(x_disp);
   u.ldb = d * es;
   u.N = d;
-  u.ntiles = cdiv(d, BN);
   u.dwA = dw1;
   u.dwB = sw ? dw3 : dw1;
   u.dw_gstride = static_cast<int64_t>(f) * d;
   u.split_row = f;
   u.partial = reinterpret_cast<float*>(ws + pl.o_part);
   u.slot_elems = static_cast<int64_t>(F) * d;
-  MOE_TRY(launch_gemm<M_DW, P_BWD_DW13>(s, dt, u));
-  MOE_TRY(launch_split_reduce(s, pl, ws, F, d, dw1, sw ? dw3 : dw1, f));
+  MOE_TRY(launch_gemm<M_DW, P_BWD_DW13>(s, dt, pl, ws, u));
+  MOE_TRY(launch_split_reduce(s, pl, ws, F, d, dw1, sw ? dw3 : dw1, f, u.dw_gstride));
 
   // dx_disp last when it fits the last-level cache (see kDxLastBytes)
   if (dx_last) MOE_TRY(launch_dx());

@@ -34,8 +34,16 @@ def test_library_exports_every_declared_symbol():
     for name in declared_functions():
         assert hasattr(lib, name), name
         assert name in B.SIGNATURES, f"binding lacks {name}"
-    assert lib.moe_abi_version() == B.ABI_VERSION == 5
+    assert lib.moe_abi_version() == B.ABI_VERSION == 6
     assert lib.moe_status_string(0) == b"MOE_OK"
+
+
+def test_set_gemm_tiles_accepts_three_modes():
+    for mode in (1, 2, 0):
+        B.moe_set_gemm_tiles(mode)
+    for bad in (-1, 3, 100):
+        assert B.lib().moe_set_gemm_tiles(bad) == EINVAL
+    B.moe_set_gemm_tiles(0)
 
 
 def test_binding_refuses_a_library_of_another_abi(monkeypatch):

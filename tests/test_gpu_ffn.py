@@ -1,6 +1,9 @@
 """GPU parity of the expert FFN (forward and backward), combine and their
 backward against the CPU oracle, through the C ABI.
 
+The bf16 cases run on both GEMM kernels (moe_set_gemm_tiles: 1 = 256x256
+tiles, 2 = 128x128 tiles, two workgroups per CU); f32 layers have one kernel.
+
 ReLU cases use dyadic inputs (x, dy in {-2..2}/4, weights in {-2..2}/16):
 every GEMM partial sum is exactly representable in fp32, so the kernels and
 the oracle agree bit for bit, including the relu'(H) decisions.  GELU and
@@ -62,7 +65,15 @@ def _oracle(rows, off, P, act, dt, E):
     return valid, fw, bw
 
 
-def _gpu(rows, cap, off, R, P, act, dt, E, d, f, rows_kind="fill"):
+def _gpu(rows, cap, off, R, P, act, dt, E, d, f, rows_kind="fill", tiles=0):
+    B.moe_set_gemm_tiles(tiles)
+    try:
+        return _gpu_run(rows, cap, off, R, P, act, dt, E, d, f, rows_kind)
+    finally:
+        B.moe_set_gemm_tiles(0)
+
+
+def _gpu_run(rows, cap, off, R, P, act, dt, E, d, f, rows_kind):
     i32 = lambda a: torch.from_numpy(np.asarray(a, dtype=np.int32)).to(dev())
     td = torch_dtype(dt)
     a = B.ACTS[act]
@@ -110,30 +121,34 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
+# (dtype, tile mode): bf16 on both kernels, f32 on its one
+DT_TILES = [("f32", 0), ("bf16", 1), ("bf16", 2)]
+
+
+@pytest.mark.parametrize("dt,tiles", DT_TILES)
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_relu_dyadic_bit_exact(dt, case):
+def test_relu_dyadic_bit_exact(dt, tiles, case):
     E, d, f, rows, slack = CASES[case]
     rows, cap, off, R, P = _problem(E, d, f, rows, slack, "relu", dt, True, 10 + case)
     valid, fw, bw = _oracle(rows, off, P, "relu", dt, E)
-    g = _gpu(rows, cap, off, R, P, "relu", dt, E, d, f)
+    g = _gpu(rows, cap, off, R, P, "relu", dt, E, d, f, tiles=tiles)
     _compare(g, valid, fw, bw, "relu", dt, exact=True)
 
 
 @pytest.mark.parametrize("act", ["gelu_tanh", "swiglu"])
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("dt,tiles", DT_TILES)
 @pytest.mark.parametrize("case", [0, 1])
-def test_gelu_swiglu_random(act, dt, case):
+def test_gelu_swiglu_random(act, dt, tiles, case):
     E, d, f, rows, slack = [(4, 192, 200, [513, 17, 0, 129], [0, 0, 4, 1]),
                             (2, 64, 136, [40, 300], [1, 1])][case]
     rows, cap, off, R, P = _problem(E, d, f, rows, slack, act, dt, False, 20 + case)
     valid, fw, bw = _oracle(rows, off, P, act, dt, E)
-    g = _gpu(rows, cap, off, R, P, act, dt, E, d, f)
+    g = _gpu(rows, cap, off, R, P, act, dt, E, d, f, tiles=tiles)
     _compare(g, valid, fw, bw, act, dt, exact=False)
 
 
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
-def test_gelu_large_preactivations(dt):
+@pytest.mark.parametrize("dt,tiles", DT_TILES)
+def test_gelu_large_preactivations(dt, tiles):
     """Pre-activations far into both tails (|H| up to about 60): the kernels'
     GELU goes through an exponential that overflows to inf on the negative
     side and must give -0 there, and H itself on the positive side."""
@@ -143,33 +158,73 @@ def test_gelu_large_preactivations(dt):
     P["w1"] = _enc(_dec(P["w1"], dt) * scale, dt)
     valid, fw, bw = _oracle(rows, off, P, "gelu_tanh", dt, E)
     assert np.abs(fw["H"]).max() > 40 and fw["H"].min() < -40
-    g = _gpu(rows, cap, off, R, P, "gelu_tanh", dt, E, d, f)
+    g = _gpu(rows, cap, off, R, P, "gelu_tanh", dt, E, d, f, tiles=tiles)
     _compare(g, valid, fw, bw, "gelu_tanh", dt, exact=False)
     a = g["h"][-1][valid]
     assert np.isfinite(a).all()
     assert (a[fw["H"] < -20] == 0).all()
 
 
-def test_split_k_weight_gradients_skewed_experts():
+@pytest.mark.parametrize("tiles", [1, 2])
+def test_split_k_weight_gradients_skewed_experts(tiles):
     """One expert holds almost every row, so the dW products split K into
     chunks and add the partial sums in a fixed order."""
     E, d, f = 8, 256, 256
     rows = [6000, 10, 0, 3, 0, 0, 77, 1]
     rows, cap, off, R, P = _problem(E, d, f, rows, [0] * E, "relu", "bf16", True, 30)
     valid, fw, bw = _oracle(rows, off, P, "relu", "bf16", E)
-    g = _gpu(rows, cap, off, R, P, "relu", "bf16", E, d, f)
+    g = _gpu(rows, cap, off, R, P, "relu", "bf16", E, d, f, tiles=tiles)
     _compare(g, valid, fw, bw, "relu", "bf16", exact=True)
 
 
-def test_padded_static_rows_match_on_filled_rows():
+@pytest.mark.parametrize("tiles", [1, 2])
+def test_split_k_swiglu_later_experts(tiles):
+    """SwiGLU weight gradients with split K on experts other than the first,
+    one of them in the upper half: [dW1; dW3] has 2f rows per expert while
+    dW1 and dW3 hold f each, so the split-K reduction must step from expert
+    to expert by f x d (a stride of 2f x d wrote expert g's sums into expert
+    2g's place, past the buffer for g >= E/2)."""
+    E, d, f = 4, 128, 136
+    rows, cap, off, R, P = _problem(E, d, f, [10, 3000, 0, 2500], [0, 2, 0, 1], "swiglu", "bf16",
+                                    False, 80)
+    valid, fw, bw = _oracle(rows, off, P, "swiglu", "bf16", E)
+    g = _gpu(rows, cap, off, R, P, "swiglu", "bf16", E, d, f, tiles=tiles)
+    _compare(g, valid, fw, bw, "swiglu", "bf16", exact=False)
+
+
+@pytest.mark.parametrize("tiles", [1, 2])
+def test_padded_static_rows_match_on_filled_rows(tiles):
     """rows = capacity (padded static-shape baseline): filled rows give the
     same results as rows = fill."""
     E, d, f = 3, 64, 128
     rows, cap, off, R, P = _problem(E, d, f, [50, 5, 100], [30, 60, 0], "relu", "bf16", True, 40)
     valid, fw, bw = _oracle(rows, off, P, "relu", "bf16", E)
-    g = _gpu(rows, cap, off, R, P, "relu", "bf16", E, d, f, rows_kind="capacity")
+    g = _gpu(rows, cap, off, R, P, "relu", "bf16", E, d, f, rows_kind="capacity", tiles=tiles)
     np.testing.assert_array_equal(g["y"][valid], fw["Y"])
     np.testing.assert_array_equal(g["dx"][valid], bw["dX"])
+
+
+@pytest.mark.parametrize("act", ["relu", "gelu_tanh", "swiglu"])
+def test_tile_kernels_bit_identical(act):
+    """The 256x256 and the 128x128 kernels add every output's products in the
+    same order (K steps of 64 in order, two MFMA k-halves per step, the same
+    split-K segments), so on random bf16 inputs every output is identical bit
+    for bit, and the automatic choice equals both.  Shapes ragged in M, N and
+    K with empty, one-row and split-K experts; the backward of the SwiGLU
+    case also runs dX with its W3 half starting at k = f."""
+    E, d, f = 6, 392, 648
+    rows = [700, 1, 0, 129, 300, 5000]
+    rows, cap, off, R, P = _problem(E, d, f, rows, [3, 0, 1, 0, 2, 0], act, "bf16", False, 70)
+    gs = [_gpu(rows, cap, off, R, P, act, "bf16", E, d, f, tiles=t) for t in (1, 2, 0)]
+    valid = np.concatenate([np.arange(off[e], off[e] + rows[e]) for e in range(E)])
+    for name in ("h", "y", "dx", "dw1", "dw2", "dw3"):
+        if gs[0][name] is None:
+            continue
+        a = gs[0][name][:, valid] if name == "h" else (gs[0][name][valid] if name in ("y", "dx") else gs[0][name])
+        for g in gs[1:]:
+            b = g[name][:, valid] if name == "h" else (g[name][valid] if name in ("y", "dx") else g[name])
+            np.testing.assert_array_equal(a, b, err_msg=name)
+    assert np.isfinite(gs[0]["dw1"]).all()
 
 
 # ---- combine, combine backward, dispatch backward -----------------------------
