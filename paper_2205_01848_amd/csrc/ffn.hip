@@ -824,10 +824,12 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_f32_kernel(const GemmPar
             q3[n].to_f(h3);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
+              // d silu(h1) h3 / dh1 = h3 sg (1 + h1 (1 - sg)), d / dh3 = h1 sg
               const float da = strip[r * kStripPitch + c8 + e];
               const float sg = sigm(h1[e]);
-              g1[e] = da * h3[e] * sg * (1.f + h1[e] * (1.f - sg));
-              g3[e] = da * h1[e] * sg;
+              const float t = da * sg, u = t * h3[e];
+              g1[e] = __builtin_fmaf(u, __builtin_fmaf(-h1[e], sg, h1[e]), u);
+              g3[e] = t * h1[e];
             }
             store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
             store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(p.f + gc) * ES, g3);
@@ -1555,17 +1557,23 @@ __global__ __launch_bounds__(kThreads16, C::kMinBlocks) void ffn_gemm16_kernel(c
           const int lm = wr0 + 16 * i + r;
           const int gc = n0 + wn * U + u8;
           if (lm < m_valid && gc < p.N) {
+            // H1 and H3 rounded to bf16 once: the packed bits are stored and
+            // their values feed the activation
             float h1[8], h3[8], a[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-              h1[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kP + u8 + e]));
-              h3[e] = Elem<T>::to_f(Elem<T>::from_f(strip[r * kP + U + u8 + e]));
-              a[e] = h1[e] * sigm(h1[e]) * h3[e];
+              h1[e] = strip[r * kP + u8 + e];
+              h3[e] = strip[r * kP + U + u8 + e];
             }
+            const uint4 b1 = pack8(h1), b3 = pack8(h3);
+            unpack8(b1, h1);
+            unpack8(b3, h3);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) a[e] = h1[e] * sigm(h1[e]) * h3[e];
             const int64_t grow = row0 + lm;
             if (p.H1) {
-              store_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h1);
-              store_vec<T>(p.H3 + grow * p.ldh + static_cast<int64_t>(gc) * ES, h3);
+              *reinterpret_cast<uint4*>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES) = b1;
+              *reinterpret_cast<uint4*>(p.H3 + grow * p.ldh + static_cast<int64_t>(gc) * ES) = b3;
             }
             store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, a);
           }
@@ -1613,10 +1621,12 @@ __global__ __launch_bounds__(kThreads16, C::kMinBlocks) void ffn_gemm16_kernel(c
             q3[n % kRing].to_f(h3);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
+              // d silu(h1) h3 / dh1 = h3 sg (1 + h1 (1 - sg)), d / dh3 = h1 sg
               const float da = strip[r * kP + c8 + e];
               const float sg = sigm(h1[e]);
-              g1[e] = da * h3[e] * sg * (1.f + h1[e] * (1.f - sg));
-              g3[e] = da * h1[e] * sg;
+              const float t = da * sg, u = t * h3[e];
+              g1[e] = __builtin_fmaf(u, __builtin_fmaf(-h1[e], sg, h1[e]), u);
+              g3[e] = t * h1[e];
             }
             store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, g1);
             store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(p.f + gc) * ES, g3);
@@ -1650,13 +1660,22 @@ __global__ __launch_bounds__(kThreads16, C::kMinBlocks) void ffn_gemm16_kernel(c
               for (int e = 0; e < 8; ++e) v[e] = sp[e];
               const int64_t grow = row0 + lm;
               if constexpr (MODE == M_FWD1) {
-                float hh[8];
+                if constexpr (ACT == ACT_RELU) {
+                  // ReLU commutes with the rounding to bf16 (round(max(h, 0)) =
+                  // max(round(h), 0)), and ReLU layers keep A alone
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  hh[e] = Elem<T>::to_f(Elem<T>::from_f(v[e]));
-                  v[e] = act_f(hh[e], ACT);
+                  for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+                } else {
+                  // H rounded to bf16 once: the packed bits are stored and
+                  // their values feed the activation
+                  const uint4 hb = pack8(v);
+                  float hh[8];
+                  unpack8(hb, hh);
+#pragma unroll
+                  for (int e = 0; e < 8; ++e) v[e] = act_f(hh[e], ACT);
+                  if (p.H1)
+                    *reinterpret_cast<uint4*>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES) = hb;
                 }
-                if (p.H1) store_vec<T>(p.H1 + grow * p.ldh + static_cast<int64_t>(gc) * ES, hh);
               }
               store_vec<T>(p.C + grow * p.ldc + static_cast<int64_t>(gc) * ES, v);
             }

@@ -43,10 +43,14 @@ def source_hash() -> str:
 
 
 def short_name(name: str) -> str:
-    # bf16 products: ffn_gemm16_kernel<MODE, PASS>; fp32: ffn_gemm_f32_kernel<MODE, PASS>
-    m = re.search(r"ffn_gemm(16|_f32)_kernel<(\d+), (\d+)>", name)
+    # bf16 products: ffn_gemm16_kernel<MODE, PASS, Tile16<RB, CB, MINB>> (the
+    # 128x128-tile instances, Tile16<4, 4, 2>, named with a _t128 suffix);
+    # fp32: ffn_gemm_f32_kernel<MODE, PASS>
+    m = re.search(r"ffn_gemm(16|_f32)_kernel<(\d+), (\d+)[,>]", name)
     if m:
-        return PASS_NAMES[int(m.group(3))] + ("_f32" if m.group(1) == "_f32" else "")
+        small = re.search(r"Tile16<4, 4, 2>", name) is not None
+        return (PASS_NAMES[int(m.group(3))] + ("_f32" if m.group(1) == "_f32" else "")
+                + ("_t128" if small else ""))
     m = re.search(r"moe::(?:\(anonymous namespace\)::)?(\w+)(<[^(]*>)?", name)
     if m:
         targs = (m.group(2) or "").replace("unsigned short", "bf16").replace("float", "f32")
