@@ -389,6 +389,14 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
   }
 }
 
+// dx is the layer's last output of a step and is not read again by the
+// library: it is stored non-temporally, so its lines do not stay dirty in
+// the caches, to be written back while the next kernels stream their inputs.
+__device__ __forceinline__ void store_stream(uint4* p, const uint4& v) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(p));
+}
+
 // dx[t] = sum_j kept dx_disp[r_j] on the cached path (no gate term): one
 // wavefront per token streams its whole rows, as the combine does (summed in
 // float32 in order j, one rounding).
@@ -420,7 +428,7 @@ __global__ __launch_bounds__(256) void row_sum_kernel(
         for (int i = 0; i < V; ++i) acc[i] += f[i];
       }
     }
-    o[v] = Elem<T>::store(acc);
+    store_stream(o + v, Elem<T>::store(acc));
   }
 }
 
@@ -504,7 +512,7 @@ __global__ __launch_bounds__(256) void dispatch_bwd_kernel(
     }
 #pragma unroll
     for (int u = 0; u < kTokGroup; ++u)
-      if (tg + u < Ttok) dx[static_cast<size_t>(tg + u) * nvec + v] = Elem<T>::store(acc[u]);
+      if (tg + u < Ttok) store_stream(dx + static_cast<size_t>(tg + u) * nvec + v, Elem<T>::store(acc[u]));
   }
 }
 
