@@ -25,6 +25,7 @@
 // per wavefront on its fp32 accumulators, staged 16 rows at a time through a
 // private LDS strip, and write 16-byte vectors.
 
+#include <algorithm>
 #include <type_traits>
 
 #include "common.hpp"
@@ -1880,13 +1881,20 @@ moe_status launch_gemm(hipStream_t s, moe_dtype dt, const FfnPlan& pl, char* ws,
   p.ntiles = cdiv(p.N, GATED ? tn / 2 : tn);
   if (VARK) p.mtiles_out = cdiv(p.M_out, tm);
   if (small) p.mtile = reinterpret_cast<const int2*>(ws + pl.o_mtile_s);
+  // the persistent grid, or fewer workgroups (a multiple of 8, for the XCD
+  // mapping) when even the most tiles the schedule can list are fewer
+  const int64_t max_items = VARK ? static_cast<int64_t>(pl.max_segs) * p.mtiles_out * p.ntiles
+                                 : static_cast<int64_t>(small ? pl.max_mtiles_s : pl.max_mtiles) *
+                                       p.ntiles;
+  const int64_t full = (small ? 2 : 1) * static_cast<int64_t>(persistent_grid());
+  const int grid = static_cast<int>(std::min(full, std::max<int64_t>(kXcds, (max_items + kXcds - 1) / kXcds * kXcds)));
   MOE_TIMED(pass_name(PASS), s);
   if (dt == MOE_BF16 && small)
-    ffn_gemm16_kernel<MODE, PASS, TileSmall><<<2 * persistent_grid(), kThreads16, 0, s>>>(p);
+    ffn_gemm16_kernel<MODE, PASS, TileSmall><<<grid, kThreads16, 0, s>>>(p);
   else if (dt == MOE_BF16)
-    ffn_gemm16_kernel<MODE, PASS, TileBig><<<persistent_grid(), kThreads16, 0, s>>>(p);
+    ffn_gemm16_kernel<MODE, PASS, TileBig><<<grid, kThreads16, 0, s>>>(p);
   else
-    ffn_gemm_f32_kernel<MODE, PASS><<<persistent_grid(), kThreads, 0, s>>>(p);
+    ffn_gemm_f32_kernel<MODE, PASS><<<grid, kThreads, 0, s>>>(p);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }
