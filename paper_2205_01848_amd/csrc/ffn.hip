@@ -3,12 +3,15 @@
 //
 // Every product is one persistent grouped GEMM kernel in "NT" form,
 //     C[m, n] = sum_k A[m, k] * B[n, k]     (both operands K-contiguous),
-// 256x256 output tiles, K tiles of 128 bytes, operand tiles loaded HBM ->
-// LDS by buffer loads, double-buffered, with an XOR swizzle that keeps the
-// MFMA fragment reads bank-conflict free.
-//  * bf16 layers: 4 wavefronts of 128x128 on v_mfma_f32_16x16x32_bf16, two
-//    barriers per K step, loads and fragment reads issued one at a time
-//    between the MFMAs (ffn_gemm16_kernel).
+// K tiles of 128 bytes, operand tiles loaded HBM -> LDS by buffer loads,
+// double-buffered, with an XOR swizzle that keeps the MFMA fragment reads
+// bank-conflict free.
+//  * bf16 layers: 4 wavefronts on v_mfma_f32_16x16x32_bf16, two barriers
+//    per K step, loads and fragment reads issued one at a time between the
+//    MFMAs (ffn_gemm16_kernel), on 256x256 tiles (waves of 128x128, one
+//    workgroup per CU) or, for products with few tiles per CU, 128x128
+//    tiles (waves of 64x64, two workgroups per CU); both add every output's
+//    products in the same order.
 //  * fp32 layers: 8 wavefronts of 128x64 on v_mfma_f32_32x32x2f32 in two
 //    ping-pong teams, one team's MFMAs overlapping the other's LDS reads
 //    (ffn_gemm_f32_kernel).
