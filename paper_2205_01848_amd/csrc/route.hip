@@ -279,114 +279,82 @@ __global__ __launch_bounds__(256) void route_rank_kernel(
 }
 
 // Token-major row kernels: one wavefront per token, `nvec` 16-byte vectors
-// per row (row bytes / 16), lanes stride over the row.
+// per row (row bytes / 16), lanes stride over the row. The token index and
+// its picks are wave-uniform (scalar registers, scalar branches); each lane
+// loads a batch of its vectors before it uses any of them (one memory
+// latency per batch instead of one per 1 KB of the row), the ragged end of a
+// row in smaller batches.
 constexpr int kRowWaves = 4;
+constexpr int kRowBatch = 4;
+
+__device__ __forceinline__ int row_token() {
+  return __builtin_amdgcn_readfirstlane(static_cast<int>(blockIdx.x) * kRowWaves +
+                                        (static_cast<int>(threadIdx.x) >> 6));
+}
+
+// Makes a loaded value opaque to the optimiser, so that the copies below
+// store the registers the batch loaded rather than loading them again per
+// kept pick.
+__device__ __forceinline__ void hold(uint4& v) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 r = __builtin_bit_cast(u32x4, v);
+  asm volatile("" : "+v"(r));
+  v = __builtin_bit_cast(uint4, r);
+}
+
+// Walks a lane's vectors v = lane, lane+64, ... < nvec in batches: f(NB, v)
+// takes vectors v, v+64, ..., v+64*(NB-1), all in range. Batches of UB while
+// they fit, then one of 2 (UB > 2), then single vectors.
+template <int UB, typename F>
+__device__ __forceinline__ void for_row_batches(int nvec, int lane, F&& f) {
+  int v = lane;
+  for (; v + 64 * (UB - 1) < nvec; v += 64 * UB) f(std::integral_constant<int, UB>{}, v);
+  if constexpr (UB > 2) {
+    if (v + 64 < nvec) {
+      f(std::integral_constant<int, 2>{}, v);
+      v += 128;
+    }
+  }
+  for (; v < nvec; v += 64) f(std::integral_constant<int, 1>{}, v);
+}
+
+template <int NB>
+__device__ __forceinline__ void gather_vecs(const uint4* __restrict__ xr, const int (&dst)[kMaxK],
+                                            int nvec, int v, uint4* __restrict__ x_disp) {
+  uint4 val[NB];
+#pragma unroll
+  for (int u = 0; u < NB; ++u) val[u] = xr[v + 64 * u];
+#pragma unroll
+  for (int u = 0; u < NB; ++u) hold(val[u]);
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    if (dst[j] >= 0) {
+      uint4* o = x_disp + static_cast<size_t>(dst[j]) * nvec + v;
+#pragma unroll
+      for (int u = 0; u < NB; ++u) o[64 * u] = val[u];
+    }
+  }
+}
 
 // Dispatch step 4: x_disp[dest_row[t,j]] = x[t] for every kept j.
 __global__ __launch_bounds__(256) void gather_rows_kernel(
     const uint4* __restrict__ x, const int32_t* __restrict__ dest_row, int T, int k,
     int nvec, uint4* __restrict__ x_disp) {
-  const int t = blockIdx.x * kRowWaves + (threadIdx.x >> 6);
+  const int t = row_token();
   const int lane = threadIdx.x & 63;
   if (t >= T) return;
   int dst[kMaxK];
   bool any = false;
 #pragma unroll
   for (int j = 0; j < kMaxK; ++j) {
-    dst[j] = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
+    dst[j] = __builtin_amdgcn_readfirstlane(j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1);
     any |= dst[j] >= 0;
   }
   if (!any) return;
   const uint4* xr = x + static_cast<size_t>(t) * nvec;
-  for (int v = lane; v < nvec; v += 64) {
-    const uint4 val = xr[v];
-#pragma unroll
-    for (int j = 0; j < kMaxK; ++j)
-      if (dst[j] >= 0) x_disp[static_cast<size_t>(dst[j]) * nvec + v] = val;
-  }
-}
-
-// y[t] = sum_j kept w[t,j] * y_disp[dest_row[t,j]]  (fp32 sum in order j)
-template <typename T>
-__global__ __launch_bounds__(256) void combine_kernel(
-    const uint4* __restrict__ yd, const int32_t* __restrict__ dest_row,
-    const float* __restrict__ wts, int Ttok, int k, int nvec, int64_t rows_alloc,
-    uint4* __restrict__ y) {
-  constexpr int V = Elem<T>::kVec;
-  const int t = blockIdx.x * kRowWaves + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (t >= Ttok) return;
-  int dst[kMaxK];
-  float w[kMaxK];
-#pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
-    dst[j] = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
-    if (dst[j] >= rows_alloc) dst[j] = -1;  // not a row of y_disp: treated as dropped
-    w[j] = j < k ? wts[static_cast<size_t>(t) * k + j] : 0.f;
-  }
-  uint4* yr = y + static_cast<size_t>(t) * nvec;
-  for (int v = lane; v < nvec; v += 64) {
-    float acc[V];
-#pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] = 0.f;
-#pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-      if (dst[j] >= 0) {
-        float f[V];
-        Elem<T>::load(yd[static_cast<size_t>(dst[j]) * nvec + v], f);
-#pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] = fmaf(w[j], f[i], acc[i]);
-      }
-    }
-    yr[v] = Elem<T>::store(acc);
-  }
-}
-
-// dweights[t,j] = <dy[t], y_disp[r]>; dy_disp[r] = w[t,j] * dy[t]
-template <typename T>
-__global__ __launch_bounds__(256) void combine_bwd_kernel(
-    const uint4* __restrict__ dy, const uint4* __restrict__ yd,
-    const int32_t* __restrict__ dest_row, const float* __restrict__ wts, int Ttok, int k,
-    int nvec, int64_t rows_alloc, uint4* __restrict__ dyd, float* __restrict__ dweights) {
-  constexpr int V = Elem<T>::kVec;
-  const int t = blockIdx.x * kRowWaves + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (t >= Ttok) return;
-  int dst[kMaxK];
-  float w[kMaxK], dot[kMaxK];
-#pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
-    dst[j] = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
-    if (dst[j] >= rows_alloc) dst[j] = -1;  // not a row of the grouped buffers
-    w[j] = j < k ? wts[static_cast<size_t>(t) * k + j] : 0.f;
-    dot[j] = 0.f;
-  }
-  const uint4* dr = dy + static_cast<size_t>(t) * nvec;
-  for (int v = lane; v < nvec; v += 64) {
-    float g[V];
-    Elem<T>::load(dr[v], g);
-#pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-      if (dst[j] >= 0) {
-        float f[V], o[V];
-        const size_t ro = static_cast<size_t>(dst[j]) * nvec + v;
-        Elem<T>::load(yd[ro], f);
-#pragma unroll
-        for (int i = 0; i < V; ++i) {
-          dot[j] = fmaf(g[i], f[i], dot[j]);
-          o[i] = w[j] * g[i];
-        }
-        dyd[ro] = Elem<T>::store(o);
-      }
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
-    if (j < k) {
-      const float s = wave_sum(dot[j]);
-      if (lane == 0) dweights[static_cast<size_t>(t) * k + j] = dst[j] >= 0 ? s : 0.f;
-    }
-  }
+  for_row_batches<kRowBatch>(nvec, lane, [&](auto nb, int v) {
+    gather_vecs<decltype(nb)::value>(xr, dst, nvec, v, x_disp);
+  });
 }
 
 // dx is the layer's last output of a step and is not read again by the
@@ -397,39 +365,168 @@ __device__ __forceinline__ void store_stream(uint4* p, const uint4& v) {
   __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(p));
 }
 
-// dx[t] = sum_j kept dx_disp[r_j] on the cached path (no gate term): one
-// wavefront per token streams its whole rows, as the combine does (summed in
-// float32 in order j, one rounding).
-template <typename T>
-__global__ __launch_bounds__(256) void row_sum_kernel(
-    const uint4* __restrict__ dxd, const int32_t* __restrict__ dest_row, int Ttok, int k,
-    int nvec, int64_t rows_alloc, uint4* __restrict__ dx) {
+// Batch of the combine below: NB vectors of the row (v, v+64, ...), all
+// kept rows' loads issued first, each output element summed in order j;
+// STREAM stores the result non-temporally.
+template <typename T, int KT, int NB, bool STREAM = false>
+__device__ __forceinline__ void combine_vecs(const uint4* __restrict__ yd, const int (&dst)[KT],
+                                             const float (&w)[KT], int nvec, int v,
+                                             uint4* __restrict__ yr) {
   constexpr int V = Elem<T>::kVec;
-  const int t = blockIdx.x * kRowWaves + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (t >= Ttok) return;
-  int dst[kMaxK];
+  uint4 raw[NB][KT];
 #pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
-    dst[j] = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
-    if (dst[j] >= rows_alloc) dst[j] = -1;
+  for (int j = 0; j < KT; ++j) {
+    if (dst[j] >= 0) {
+      const uint4* src = yd + static_cast<size_t>(dst[j]) * nvec + v;
+#pragma unroll
+      for (int u = 0; u < NB; ++u) raw[u][j] = src[64 * u];
+    }
   }
-  uint4* o = dx + static_cast<size_t>(t) * nvec;
-  for (int v = lane; v < nvec; v += 64) {
+#pragma unroll
+  for (int u = 0; u < NB; ++u) {
     float acc[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) acc[i] = 0.f;
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
+    for (int j = 0; j < KT; ++j) {
       if (dst[j] >= 0) {
         float f[V];
-        Elem<T>::load(dxd[static_cast<size_t>(dst[j]) * nvec + v], f);
+        Elem<T>::load(raw[u][j], f);
 #pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] += f[i];
+        for (int i = 0; i < V; ++i) acc[i] = fmaf(w[j], f[i], acc[i]);
       }
     }
-    store_stream(o + v, Elem<T>::store(acc));
+    if (STREAM)
+      store_stream(yr + v + 64 * u, Elem<T>::store(acc));
+    else
+      yr[v + 64 * u] = Elem<T>::store(acc);
   }
+}
+
+// y[t] = sum_j kept w[t,j] * y_disp[dest_row[t,j]]  (fp32 sum in order j);
+// KT >= k bounds the picks held in registers, and the batch shrinks as KT
+// grows (KT rows' vectors per batch element).
+template <typename T, int KT>
+__global__ __launch_bounds__(256) void combine_kernel(
+    const uint4* __restrict__ yd, const int32_t* __restrict__ dest_row,
+    const float* __restrict__ wts, int Ttok, int k, int nvec, int64_t rows_alloc,
+    uint4* __restrict__ y) {
+  const int t = row_token();
+  const int lane = threadIdx.x & 63;
+  if (t >= Ttok) return;
+  int dst[KT];
+  float w[KT];
+#pragma unroll
+  for (int j = 0; j < KT; ++j) {
+    int r = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
+    if (r >= rows_alloc) r = -1;  // not a row of y_disp: treated as dropped
+    dst[j] = __builtin_amdgcn_readfirstlane(r);
+    w[j] = j < k ? wts[static_cast<size_t>(t) * k + j] : 0.f;
+  }
+  uint4* yr = y + static_cast<size_t>(t) * nvec;
+  constexpr int UB = KT <= 2 ? kRowBatch : (KT <= 4 ? 2 : 1);
+  for_row_batches<UB>(nvec, lane, [&](auto nb, int v) {
+    combine_vecs<T, KT, decltype(nb)::value>(yd, dst, w, nvec, v, yr);
+  });
+}
+
+// Batch of the combine backward below: NB vectors of dy[t] and of each kept
+// row of y_disp, loads first; dot[j] accumulates in the lane's vector order.
+template <typename T, int KT, int NB>
+__device__ __forceinline__ void combine_bwd_vecs(const uint4* __restrict__ dr,
+                                                 const uint4* __restrict__ yd,
+                                                 const int (&dst)[KT], const float (&w)[KT],
+                                                 float (&dot)[KT], int nvec, int v,
+                                                 uint4* __restrict__ dyd) {
+  constexpr int V = Elem<T>::kVec;
+  uint4 rg[NB], ry[NB][KT];
+#pragma unroll
+  for (int u = 0; u < NB; ++u) rg[u] = dr[v + 64 * u];
+#pragma unroll
+  for (int j = 0; j < KT; ++j) {
+    if (dst[j] >= 0) {
+      const uint4* src = yd + static_cast<size_t>(dst[j]) * nvec + v;
+#pragma unroll
+      for (int u = 0; u < NB; ++u) ry[u][j] = src[64 * u];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < NB; ++u) {
+    float g[V];
+    Elem<T>::load(rg[u], g);
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      if (dst[j] >= 0) {
+        float f[V], o[V];
+        Elem<T>::load(ry[u][j], f);
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+          dot[j] = fmaf(g[i], f[i], dot[j]);
+          o[i] = w[j] * g[i];
+        }
+        dyd[static_cast<size_t>(dst[j]) * nvec + v + 64 * u] = Elem<T>::store(o);
+      }
+    }
+  }
+}
+
+// dweights[t,j] = <dy[t], y_disp[r]>; dy_disp[r] = w[t,j] * dy[t]
+template <typename T, int KT>
+__global__ __launch_bounds__(256) void combine_bwd_kernel(
+    const uint4* __restrict__ dy, const uint4* __restrict__ yd,
+    const int32_t* __restrict__ dest_row, const float* __restrict__ wts, int Ttok, int k,
+    int nvec, int64_t rows_alloc, uint4* __restrict__ dyd, float* __restrict__ dweights) {
+  const int t = row_token();
+  const int lane = threadIdx.x & 63;
+  if (t >= Ttok) return;
+  int dst[KT];
+  float w[KT], dot[KT];
+#pragma unroll
+  for (int j = 0; j < KT; ++j) {
+    int r = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
+    if (r >= rows_alloc) r = -1;  // not a row of the grouped buffers
+    dst[j] = __builtin_amdgcn_readfirstlane(r);
+    w[j] = j < k ? wts[static_cast<size_t>(t) * k + j] : 0.f;
+    dot[j] = 0.f;
+  }
+  const uint4* dr = dy + static_cast<size_t>(t) * nvec;
+  constexpr int UB = KT <= 2 ? kRowBatch : (KT <= 4 ? 2 : 1);
+  for_row_batches<UB>(nvec, lane, [&](auto nb, int v) {
+    combine_bwd_vecs<T, KT, decltype(nb)::value>(dr, yd, dst, w, dot, nvec, v, dyd);
+  });
+#pragma unroll
+  for (int j = 0; j < KT; ++j) {
+    if (j < k) {
+      const float s = wave_sum(dot[j]);
+      if (lane == 0) dweights[static_cast<size_t>(t) * k + j] = dst[j] >= 0 ? s : 0.f;
+    }
+  }
+}
+
+// dx[t] = sum_j kept dx_disp[r_j] on the cached path (no gate term): the
+// combine with unit weights (fmaf(1, f, acc) rounds as acc + f does), summed
+// in float32 in order j, one rounding, stored non-temporally.
+template <typename T, int KT>
+__global__ __launch_bounds__(256) void row_sum_kernel(
+    const uint4* __restrict__ dxd, const int32_t* __restrict__ dest_row, int Ttok, int k,
+    int nvec, int64_t rows_alloc, uint4* __restrict__ dx) {
+  const int t = row_token();
+  const int lane = threadIdx.x & 63;
+  if (t >= Ttok) return;
+  int dst[KT];
+  float w[KT];
+#pragma unroll
+  for (int j = 0; j < KT; ++j) {
+    int r = j < k ? dest_row[static_cast<size_t>(t) * k + j] : -1;
+    if (r >= rows_alloc) r = -1;
+    dst[j] = __builtin_amdgcn_readfirstlane(r);
+    w[j] = 1.f;
+  }
+  uint4* o = dx + static_cast<size_t>(t) * nvec;
+  constexpr int UB = KT <= 2 ? kRowBatch : (KT <= 4 ? 2 : 1);
+  for_row_batches<UB>(nvec, lane, [&](auto nb, int v) {
+    combine_vecs<T, KT, decltype(nb)::value, true>(dxd, dst, w, nvec, v, o);
+  });
 }
 
 // dx[t] = sum_j kept dx_disp[r_j] + dl[t] . w_g.  A wavefront takes a group
@@ -752,6 +849,17 @@ extern "C" moe_status moe_dispatch_noalloc(void* stream, moe_dtype dt, int T, in
                          dest_row, src, x_disp, status, ws);
 }
 
+// Calls f with std::integral_constant<int, KT> for the smallest pick bound
+// KT in {1, 2, 4, 8} with k <= KT (templated row kernels size their per-pick
+// registers by KT).
+template <typename F>
+static void with_pick_bound(int k, F&& f) {
+  if (k <= 1) f(std::integral_constant<int, 1>{});
+  else if (k <= 2) f(std::integral_constant<int, 2>{});
+  else if (k <= 4) f(std::integral_constant<int, 4>{});
+  else f(std::integral_constant<int, 8>{});
+}
+
 extern "C" moe_status moe_combine(void* stream, moe_dtype dt, int T, int d, int k,
                                   int64_t rows_alloc, const void* y_disp,
                                   const int32_t* dest_row, const float* weights, void* y) {
@@ -763,14 +871,17 @@ extern "C" moe_status moe_combine(void* stream, moe_dtype dt, int T, int d, int 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
   MOE_TIMED("combine", s);
-  if (dt == MOE_BF16)
-    combine_kernel<uint16_t><<<nblocks(T, kRowWaves), 256, 0, s>>>(
-        static_cast<const uint4*>(y_disp), dest_row, weights, T, k, nvec, rows_alloc,
-        static_cast<uint4*>(y));
-  else
-    combine_kernel<float><<<nblocks(T, kRowWaves), 256, 0, s>>>(
-        static_cast<const uint4*>(y_disp), dest_row, weights, T, k, nvec, rows_alloc,
-        static_cast<uint4*>(y));
+  with_pick_bound(k, [&](auto kt_tag) {
+    constexpr int KT = decltype(kt_tag)::value;
+    if (dt == MOE_BF16)
+      combine_kernel<uint16_t, KT><<<nblocks(T, kRowWaves), 256, 0, s>>>(
+          static_cast<const uint4*>(y_disp), dest_row, weights, T, k, nvec, rows_alloc,
+          static_cast<uint4*>(y));
+    else
+      combine_kernel<float, KT><<<nblocks(T, kRowWaves), 256, 0, s>>>(
+          static_cast<const uint4*>(y_disp), dest_row, weights, T, k, nvec, rows_alloc,
+          static_cast<uint4*>(y));
+  });
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }
@@ -787,14 +898,17 @@ extern "C" moe_status moe_combine_bwd(void* stream, moe_dtype dt, int T, int d, 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nvec = static_cast<int>(static_cast<int64_t>(d) * esize(dt) / 16);
   MOE_TIMED("combine_bwd", s);
-  if (dt == MOE_BF16)
-    combine_bwd_kernel<uint16_t><<<nblocks(T, kRowWaves), 256, 0, s>>>(
-        static_cast<const uint4*>(dy), static_cast<const uint4*>(y_disp), dest_row, weights, T,
-        k, nvec, rows_alloc, static_cast<uint4*>(dy_disp), dweights);
-  else
-    combine_bwd_kernel<float><<<nblocks(T, kRowWaves), 256, 0, s>>>(
-        static_cast<const uint4*>(dy), static_cast<const uint4*>(y_disp), dest_row, weights, T,
-        k, nvec, rows_alloc, static_cast<uint4*>(dy_disp), dweights);
+  with_pick_bound(k, [&](auto kt_tag) {
+    constexpr int KT = decltype(kt_tag)::value;
+    if (dt == MOE_BF16)
+      combine_bwd_kernel<uint16_t, KT><<<nblocks(T, kRowWaves), 256, 0, s>>>(
+          static_cast<const uint4*>(dy), static_cast<const uint4*>(y_disp), dest_row, weights,
+          T, k, nvec, rows_alloc, static_cast<uint4*>(dy_disp), dweights);
+    else
+      combine_bwd_kernel<float, KT><<<nblocks(T, kRowWaves), 256, 0, s>>>(
+          static_cast<const uint4*>(dy), static_cast<const uint4*>(y_disp), dest_row, weights,
+          T, k, nvec, rows_alloc, static_cast<uint4*>(dy_disp), dweights);
+  });
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }
@@ -816,12 +930,15 @@ extern "C" moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d,
   uint4* o = static_cast<uint4*>(dx);
   MOE_TIMED("dispatch_bwd", s);
   if (!dlogits) {
-    if (dt == MOE_BF16)
-      row_sum_kernel<uint16_t><<<nblocks(T, kRowWaves), 256, 0, s>>>(a, dest_row, T, k, nvec,
-                                                                    rows_alloc, o);
-    else
-      row_sum_kernel<float><<<nblocks(T, kRowWaves), 256, 0, s>>>(a, dest_row, T, k, nvec,
-                                                                 rows_alloc, o);
+    with_pick_bound(k, [&](auto kt_tag) {
+      constexpr int KT = decltype(kt_tag)::value;
+      if (dt == MOE_BF16)
+        row_sum_kernel<uint16_t, KT><<<nblocks(T, kRowWaves), 256, 0, s>>>(a, dest_row, T, k,
+                                                                          nvec, rows_alloc, o);
+      else
+        row_sum_kernel<float, KT><<<nblocks(T, kRowWaves), 256, 0, s>>>(a, dest_row, T, k,
+                                                                       nvec, rows_alloc, o);
+    });
     MOE_LAUNCH_CHECK();
     return MOE_OK;
   }
@@ -833,10 +950,7 @@ extern "C" moe_status moe_dispatch_bwd(void* stream, moe_dtype dt, int T, int d,
     else
       dispatch_bwd_kernel<float, KT><<<grid, 256, 0, s>>>(a, dest_row, dlogits, g, T, E, k, nvec, rows_alloc, o);
   };
-  if (k <= 1) go(std::integral_constant<int, 1>{});
-  else if (k <= 2) go(std::integral_constant<int, 2>{});
-  else if (k <= 4) go(std::integral_constant<int, 4>{});
-  else go(std::integral_constant<int, 8>{});
+  with_pick_bound(k, go);
   MOE_LAUNCH_CHECK();
   return MOE_OK;
 }

@@ -229,7 +229,10 @@ def test_tile_kernels_bit_identical(act):
 
 # ---- combine, combine backward, dispatch backward -----------------------------
 @pytest.mark.parametrize("dt,k,d", [("bf16", 2, 512), ("f32", 1, 64), ("bf16", 3, 136),
-                                    ("bf16", 5, 1096), ("f32", 2, 584)])
+                                    ("bf16", 5, 1096), ("f32", 2, 584),
+                                    # rows of several 4-vector batches per lane plus a
+                                    # ragged end (513, 250 and 257 16-byte vectors)
+                                    ("bf16", 2, 4104), ("f32", 4, 1000), ("bf16", 1, 2056)])
 def test_combine_and_backward(dt, k, d):
     rng = np.random.default_rng(50 + k)
     T, E = 1500, 6

@@ -197,6 +197,20 @@ def test_dispatch_random_ids(T, E, k, cap_kind):
     _check_dispatch(_bf16_rows(T, d, 1), ids, E, cap, off, int(off[-1]))
 
 
+@pytest.mark.parametrize("dt,d", [("bf16", 4104), ("f32", 1032)])
+def test_dispatch_wide_ragged_rows(dt, d):
+    """Rows of several load batches per lane and a ragged end (513 and 258
+    16-byte vectors), with drops."""
+    rng = np.random.default_rng(d)
+    T, E, k = 700, 8, 2
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    cap = np.maximum(O.count_assignments(ids, E) * 2 // 3, 1)
+    off = O.exclusive_offsets(cap)
+    x = (_bf16_rows(T, d, 5) if dt == "bf16"
+         else rng.standard_normal((T, d)).astype(np.float32))
+    _check_dispatch(x, ids, E, cap, off, int(off[-1]), dt=dt)
+
+
 def test_dispatch_cached_zipf_ids_fp32_rows():
     wl = W.small("c4", T=6000, d=32, f=64)
     I = W.make_inputs(wl)
