@@ -100,6 +100,9 @@ def parse():
     ap.add_argument("--tiles", type=int, default=0, choices=[0, 1, 2],
                     help="bf16 GEMM tiles: 0 the library's choice per product, 1 256x256 "
                          "only, 2 128x128 only (two workgroups per CU)")
+    ap.add_argument("--dx-weight-copy", type=int, default=0, choices=[0, 1, 2],
+                    help="bf16 dX operand: 0 the library's choice, 1 W1/W3 read K-major, "
+                         "2 from a transposed copy made in the backward")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead of the layer: time a plain device-to-device copy of this "
                          "many GiB (achievable HBM bandwidth; byte-counter calibration)")
@@ -301,6 +304,11 @@ def hbm_bytes(wl, kept, active, padded=0):
         b["combine_bwd"] = T * d * s + 2 * kept * d * s + T * k * 12
         b["dispatch_bwd"] = kept * d * s + T * d * s + T * k * 4 + \
             (T * E * 4 + E * d * s if wl.gate == "linear" else 0)
+        if wl.dtype == "bf16":
+            # the transposed copy of [W1; W3] read by dX (large experts only):
+            # the weights read once and written once
+            g = 2 if wl.act == "swiglu" else 1
+            b["transpose_w"] = 2 * E * g * wl.f * d * s
     if wl.gate != "linear":
         del b["gate_fwd"]
     # operators of the variants
@@ -681,6 +689,7 @@ def main():
     from paper_2205_01848_amd import binding as B
 
     B.moe_set_gemm_tiles(args.tiles)
+    B.moe_set_dx_weight_copy(args.dx_weight_copy)
     wl = W.config(args.workload)
     cap_rule = wl.capacity[-1]
     if args.capacity:
@@ -781,7 +790,8 @@ def main():
                    "capacity": f"{cap_rule[0]} {cap_rule[1]}/{cap_rule[2]}",
                    "rows": args.rows, "pass": "fwd+bwd" if wl.backward else "fwd",
                    "row_align": L.row_align, "parallelism": "single GPU",
-                   "gemm_tiles": ["auto", "256x256", "128x128"][args.tiles]},
+                   "gemm_tiles": ["auto", "256x256", "128x128"][args.tiles],
+                   "dx_weight_copy": ["auto", "off", "on"][args.dx_weight_copy]},
         "roofline": roof,
         "cpu_baseline": None,
         "detail": {"kept_rows": kept, "executed_rows": executed, "status": status,

@@ -505,6 +505,22 @@ int moe_timing_report(char* buf, size_t len);
  */
 moe_status moe_set_gemm_tiles(int mode);
 
+/*
+ * Operand layout of the bf16 dX product of moe_expert_ffn_bwd (a tuning and
+ * testing aid; not part of the method).  dX contracts over f, the row index
+ * of w1/w3, so it reads them K-major; it can instead read a transposed copy
+ * that the call makes first in its workspace ([E, d, F] with F = 2f under
+ * SwiGLU, bf16).  mode 0 (default): the copy when the row budget holds at
+ * least 8192 rows per expert (rows_alloc >= 8192 E), where the faster
+ * product outweighs the copy; 1: never; 2: always.  The products are
+ * identical bit for bit either way.  moe_ffn_bwd_workspace_bytes includes
+ * the copy's E*d*F*2 bytes when the current mode would make it; a call
+ * whose workspace lacks them reads the weights K-major.  Process-wide; read
+ * when moe_expert_ffn_bwd (or the workspace query) is called.  Returns
+ * MOE_EINVAL for other modes. [host]
+ */
+moe_status moe_set_dx_weight_copy(int mode);
+
 #ifdef __cplusplus
 }
 #endif

@@ -73,13 +73,14 @@ SIGNATURES = {
     "moe_policy_state": (_c_int, [_p, _p, _p, _p, _p]),
     "moe_timing_enable": (_c_int, [_c_int]),
     "moe_set_gemm_tiles": (_c_int, [_c_int]),
+    "moe_set_dx_weight_copy": (_c_int, [_c_int]),
     "moe_timing_report": (_c_int, [ctypes.c_char_p, _c_size]),
 }
 
 _lib = None
 
 
-ABI_VERSION = 6   # moe_abi_version() of the library this binding is written for
+ABI_VERSION = 7   # moe_abi_version() of the library this binding is written for
 
 
 class MoEError(RuntimeError):
@@ -493,6 +494,11 @@ def moe_timing_enable(on: bool):
 def moe_set_gemm_tiles(mode: int):
     """0: automatic tile choice; 1: 256x256 tiles only; 2: 128x128 tiles only."""
     _check(lib().moe_set_gemm_tiles(int(mode)), "moe_set_gemm_tiles")
+
+
+def moe_set_dx_weight_copy(mode: int):
+    """0: automatic; 1: dX reads W1/W3 K-major; 2: dX reads a transposed copy (bf16)."""
+    _check(lib().moe_set_dx_weight_copy(int(mode)), "moe_set_dx_weight_copy")
 
 
 def moe_timing_report() -> dict:

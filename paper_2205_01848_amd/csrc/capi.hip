@@ -80,7 +80,7 @@ extern "C" const char* moe_status_string(int status) {
   }
 }
 
-extern "C" int moe_abi_version(void) { return 6; }
+extern "C" int moe_abi_version(void) { return 7; }
 
 extern "C" moe_status moe_timing_enable(int on) {
   std::lock_guard<std::mutex> lk(g_mu);

@@ -25,7 +25,7 @@ import re
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 PASS_NAMES = ["gemm_fwd_h", "gemm_fwd_y", "gemm_bwd_da", "gemm_bwd_dx", "gemm_bwd_dw2",
-              "gemm_bwd_dw13"]
+              "gemm_bwd_dw13", "gemm_bwd_dx"]
 
 
 def source_hash() -> str:

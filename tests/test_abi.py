@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared_functions():
         assert hasattr(lib, name), name
         assert name in B.SIGNATURES, f"binding lacks {name}"
-    assert lib.moe_abi_version() == B.ABI_VERSION == 6
+    assert lib.moe_abi_version() == B.ABI_VERSION == 7
     assert lib.moe_status_string(0) == b"MOE_OK"
 
 
@@ -44,6 +44,33 @@ def test_set_gemm_tiles_accepts_three_modes():
     for bad in (-1, 3, 100):
         assert B.lib().moe_set_gemm_tiles(bad) == EINVAL
     B.moe_set_gemm_tiles(0)
+
+
+def test_dx_weight_copy_modes_and_workspace():
+    """The workspace query includes the transposed copy of [W1; W3] (E d F
+    bf16 elements) exactly when the mode would make it: automatically from
+    8192 rows per expert, never under mode 1, always under mode 2, and never
+    for float32 layers."""
+    BF16, F32, SWIGLU, RELU = 1, 0, 2, 0
+    q = B.lib().moe_ffn_bwd_workspace_bytes
+    E, d, f = 4, 256, 512
+    try:
+        for act, F in ((SWIGLU, 2 * f), (RELU, f)):
+            copy = E * d * F * 2
+            B.moe_set_dx_weight_copy(1)
+            small, big = q(BF16, act, E, d, f, 8192 * E - 1), q(BF16, act, E, d, f, 8192 * E)
+            B.moe_set_dx_weight_copy(0)
+            assert q(BF16, act, E, d, f, 8192 * E - 1) == small
+            assert copy <= q(BF16, act, E, d, f, 8192 * E) - big < copy + 512
+            B.moe_set_dx_weight_copy(2)
+            assert copy <= q(BF16, act, E, d, f, 8192 * E - 1) - small < copy + 512
+            f32 = [q(F32, act, E, d, f, 8192 * E)]
+            B.moe_set_dx_weight_copy(1)
+            assert q(F32, act, E, d, f, 8192 * E) == f32[0]
+        for bad in (-1, 3):
+            assert B.lib().moe_set_dx_weight_copy(bad) == EINVAL
+    finally:
+        B.moe_set_dx_weight_copy(0)
 
 
 def test_binding_refuses_a_library_of_another_abi(monkeypatch):

@@ -2,7 +2,9 @@
 backward against the CPU oracle, through the C ABI.
 
 The bf16 cases run on both GEMM kernels (moe_set_gemm_tiles: 1 = 256x256
-tiles, 2 = 128x128 tiles, two workgroups per CU); f32 layers have one kernel.
+tiles, 2 = 128x128 tiles, two workgroups per CU) and with dX reading the
+weights K-major or from their transposed copy (moe_set_dx_weight_copy); f32
+layers have one kernel.
 
 ReLU cases use dyadic inputs (x, dy in {-2..2}/4, weights in {-2..2}/16):
 every GEMM partial sum is exactly representable in fp32, so the kernels and
@@ -65,12 +67,14 @@ def _oracle(rows, off, P, act, dt, E):
     return valid, fw, bw
 
 
-def _gpu(rows, cap, off, R, P, act, dt, E, d, f, rows_kind="fill", tiles=0):
+def _gpu(rows, cap, off, R, P, act, dt, E, d, f, rows_kind="fill", tiles=0, wcopy=0):
     B.moe_set_gemm_tiles(tiles)
+    B.moe_set_dx_weight_copy(wcopy)
     try:
         return _gpu_run(rows, cap, off, R, P, act, dt, E, d, f, rows_kind)
     finally:
         B.moe_set_gemm_tiles(0)
+        B.moe_set_dx_weight_copy(0)
 
 
 def _gpu_run(rows, cap, off, R, P, act, dt, E, d, f, rows_kind):
@@ -121,34 +125,36 @@ CASES = [
 ]
 
 
-# (dtype, tile mode): bf16 on both kernels, f32 on its one
-DT_TILES = [("f32", 0), ("bf16", 1), ("bf16", 2)]
+# (dtype, tile mode, dX weight copy): bf16 on both kernels, each with dX
+# reading the weights K-major (1) and from the transposed copy (2); f32 on
+# its one kernel
+DT_TILES = [("f32", 0, 0), ("bf16", 1, 1), ("bf16", 2, 1), ("bf16", 1, 2), ("bf16", 2, 2)]
 
 
-@pytest.mark.parametrize("dt,tiles", DT_TILES)
+@pytest.mark.parametrize("dt,tiles,wcopy", DT_TILES)
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_relu_dyadic_bit_exact(dt, tiles, case):
+def test_relu_dyadic_bit_exact(dt, tiles, wcopy, case):
     E, d, f, rows, slack = CASES[case]
     rows, cap, off, R, P = _problem(E, d, f, rows, slack, "relu", dt, True, 10 + case)
     valid, fw, bw = _oracle(rows, off, P, "relu", dt, E)
-    g = _gpu(rows, cap, off, R, P, "relu", dt, E, d, f, tiles=tiles)
+    g = _gpu(rows, cap, off, R, P, "relu", dt, E, d, f, tiles=tiles, wcopy=wcopy)
     _compare(g, valid, fw, bw, "relu", dt, exact=True)
 
 
 @pytest.mark.parametrize("act", ["gelu_tanh", "swiglu"])
-@pytest.mark.parametrize("dt,tiles", DT_TILES)
+@pytest.mark.parametrize("dt,tiles,wcopy", DT_TILES)
 @pytest.mark.parametrize("case", [0, 1])
-def test_gelu_swiglu_random(act, dt, tiles, case):
+def test_gelu_swiglu_random(act, dt, tiles, wcopy, case):
     E, d, f, rows, slack = [(4, 192, 200, [513, 17, 0, 129], [0, 0, 4, 1]),
                             (2, 64, 136, [40, 300], [1, 1])][case]
     rows, cap, off, R, P = _problem(E, d, f, rows, slack, act, dt, False, 20 + case)
     valid, fw, bw = _oracle(rows, off, P, act, dt, E)
-    g = _gpu(rows, cap, off, R, P, act, dt, E, d, f, tiles=tiles)
+    g = _gpu(rows, cap, off, R, P, act, dt, E, d, f, tiles=tiles, wcopy=wcopy)
     _compare(g, valid, fw, bw, act, dt, exact=False)
 
 
-@pytest.mark.parametrize("dt,tiles", DT_TILES)
-def test_gelu_large_preactivations(dt, tiles):
+@pytest.mark.parametrize("dt,tiles,wcopy", DT_TILES)
+def test_gelu_large_preactivations(dt, tiles, wcopy):
     """Pre-activations far into both tails (|H| up to about 60): the kernels'
     GELU goes through an exponential that overflows to inf on the negative
     side and must give -0 there, and H itself on the positive side."""
@@ -158,7 +164,7 @@ def test_gelu_large_preactivations(dt, tiles):
     P["w1"] = _enc(_dec(P["w1"], dt) * scale, dt)
     valid, fw, bw = _oracle(rows, off, P, "gelu_tanh", dt, E)
     assert np.abs(fw["H"]).max() > 40 and fw["H"].min() < -40
-    g = _gpu(rows, cap, off, R, P, "gelu_tanh", dt, E, d, f, tiles=tiles)
+    g = _gpu(rows, cap, off, R, P, "gelu_tanh", dt, E, d, f, tiles=tiles, wcopy=wcopy)
     _compare(g, valid, fw, bw, "gelu_tanh", dt, exact=False)
     a = g["h"][-1][valid]
     assert np.isfinite(a).all()
@@ -209,13 +215,16 @@ def test_tile_kernels_bit_identical(act):
     """The 256x256 and the 128x128 kernels add every output's products in the
     same order (K steps of 64 in order, two MFMA k-halves per step, the same
     split-K segments), so on random bf16 inputs every output is identical bit
-    for bit, and the automatic choice equals both.  Shapes ragged in M, N and
-    K with empty, one-row and split-K experts; the backward of the SwiGLU
+    for bit, and the automatic choice equals both; dX is the same whether it
+    reads the weights K-major or from their transposed copy.  Shapes ragged
+    in M, N and K with empty, one-row and split-K experts (d and f not
+    multiples of the 64-element copy blocks); the backward of the SwiGLU
     case also runs dX with its W3 half starting at k = f."""
     E, d, f = 6, 392, 648
     rows = [700, 1, 0, 129, 300, 5000]
     rows, cap, off, R, P = _problem(E, d, f, rows, [3, 0, 1, 0, 2, 0], act, "bf16", False, 70)
-    gs = [_gpu(rows, cap, off, R, P, act, "bf16", E, d, f, tiles=t) for t in (1, 2, 0)]
+    gs = [_gpu(rows, cap, off, R, P, act, "bf16", E, d, f, tiles=t, wcopy=c)
+          for t, c in ((1, 1), (2, 1), (0, 0), (1, 2), (2, 2))]
     valid = np.concatenate([np.arange(off[e], off[e] + rows[e]) for e in range(E)])
     for name in ("h", "y", "dx", "dw1", "dw2", "dw3"):
         if gs[0][name] is None:
