@@ -21,6 +21,10 @@
 //  * var-K products (dW): K of expert e is its row count; the K range is
 //    split into chunks only when few experts carry most rows, and split
 //    partial sums are added in a fixed order (deterministic).
+//  * operands whose contraction index is their row index (the weights in dA
+//    and dX, both operands of dW) are read K-major through transposing LDS
+//    reads; on large experts dX instead reads a transposed copy of [W1; W3]
+//    that the backward writes first.
 // The persistent grid maps workgroup b to XCD b % 8 and hands each XCD a
 // contiguous run of tiles arranged as 4 M-tiles x 8 N-tiles, so tiles that
 // share operand panels share that XCD's L2.
@@ -1705,13 +1709,9 @@ __global__ __launch_bounds__(kThreads16, C::kMinBlocks) void ffn_gemm16_kernel(c
 }
 
 // ---------------------------------------------------------------------------
-// split-K reduction
+// transposed weights
 // ---------------------------------------------------------------------------
-// dW[g] = sum over the expert's split slots, in slot order.  A bounded grid
-// strides over the elements (blockIdx.y = expert), so experts without a
-// split cost one early exit per block rather than a launch per 1024
-// elements.
-// Transposed copy of expert weights (bf16), so that dA and dX read them
+// Transposed copy of expert weights (bf16), so that dX reads them
 // K-contiguous: dst[g][n][k] = src1[g][k][n] for k < K1 and src2[g][k - K1][n]
 // for K1 <= k < K1 + K2 (dst rows of K1 + K2 elements).  A workgroup moves a
 // 64 (k) x 64 (n) block through LDS: 16-byte loads along n, 16-byte stores
@@ -1728,39 +1728,46 @@ __global__ __launch_bounds__(256) void transpose_w_kernel(const uint16_t* __rest
   const int K = K1 + K2;
   const int64_t s1 = static_cast<int64_t>(g) * K1 * N, s2 = static_cast<int64_t>(g) * K2 * N;
   for (int k0 = blockIdx.y * kTr; k0 < K; k0 += gridDim.y * kTr) {
-  __syncthreads();   // the previous block's reads of the tile are done
+    __syncthreads();   // the previous block's reads of the tile are done
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    const int kk = c >> 3, nn = (c & 7) * 8;
-    const int k = k0 + kk, n = n0 + nn;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (k < K && n < N) {
-      const uint16_t* src = k < K1 ? src1 + s1 + static_cast<int64_t>(k) * N + n
-                                   : src2 + s2 + static_cast<int64_t>(k - K1) * N + n;
-      v = *reinterpret_cast<const uint4*>(src);
+    for (int i = 0; i < 2; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int kk = c >> 3, nn = (c & 7) * 8;
+      const int k = k0 + kk, n = n0 + nn;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (k < K && n < N) {
+        const uint16_t* src = k < K1 ? src1 + s1 + static_cast<int64_t>(k) * N + n
+                                     : src2 + s2 + static_cast<int64_t>(k - K1) * N + n;
+        v = *reinterpret_cast<const uint4*>(src);
+      }
+      *reinterpret_cast<uint4*>(&tile[kk][nn]) = v;
     }
-    *reinterpret_cast<uint4*>(&tile[kk][nn]) = v;
-  }
-  __syncthreads();
+    __syncthreads();
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    const int nn = c >> 3, kk = (c & 7) * 8;
-    const int n = n0 + nn, k = k0 + kk;
-    if (n < N && k < K) {
-      uint32_t w[4];
+    for (int i = 0; i < 2; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int nn = c >> 3, kk = (c & 7) * 8;
+      const int n = n0 + nn, k = k0 + kk;
+      if (n < N && k < K) {
+        uint32_t w[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        w[j] = static_cast<uint32_t>(tile[kk + 2 * j][nn]) |
-               (static_cast<uint32_t>(tile[kk + 2 * j + 1][nn]) << 16);
-      *reinterpret_cast<uint4*>(dst + (static_cast<int64_t>(g) * N + n) * K + k) =
-          make_uint4(w[0], w[1], w[2], w[3]);
+        for (int j = 0; j < 4; ++j)
+          w[j] = static_cast<uint32_t>(tile[kk + 2 * j][nn]) |
+                 (static_cast<uint32_t>(tile[kk + 2 * j + 1][nn]) << 16);
+        *reinterpret_cast<uint4*>(dst + (static_cast<int64_t>(g) * N + n) * K + k) =
+            make_uint4(w[0], w[1], w[2], w[3]);
+      }
     }
-  }
   }
 }
 
+// ---------------------------------------------------------------------------
+// split-K reduction
+// ---------------------------------------------------------------------------
+// dW[g] = sum over the expert's split slots, in slot order.  A bounded grid
+// strides over the elements (blockIdx.y = expert), so experts without a
+// split cost one early exit per block rather than a launch per 1024
+// elements.
 constexpr int kReduceBlocks = 1024;   // blocks per expert
 
 // The slots are added in slot order; their loads are issued four at a time
