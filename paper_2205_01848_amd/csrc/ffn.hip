@@ -1918,8 +1918,13 @@ int g_tile_mode = 0;
 // kernels' tile counts as if each expert held rows_alloc / E rows, counts
 // the rounds of the persistent grids (one 256x256 tile or two 128x128
 // tiles per CU at a time), and takes the 128x128 kernel when its rounds,
-// each worth about 0.65 of a 256x256 round, take less time.
-bool use_small_tiles(const FfnPlan& pl, moe_dtype dt, bool vark, bool gated, int N, int M_out) {
+// each worth about 0.65 of a 256x256 round, take less time.  With K of 512
+// or less (8 K steps per tile) a 256x256 tile's unoverlapped prologue and
+// epilogue weigh more, and a 128x128 round is worth about 0.55 of one
+// (measured on 512 x 2048 products of 1000-row experts).  K = 0: not known
+// on the host (weight gradients).
+bool use_small_tiles(const FfnPlan& pl, moe_dtype dt, bool vark, bool gated, int N, int M_out,
+                     int K) {
   if (dt != MOE_BF16) return false;
   if (g_tile_mode == 1) return false;
   if (g_tile_mode == 2) return true;
@@ -1932,7 +1937,8 @@ bool use_small_tiles(const FfnPlan& pl, moe_dtype dt, bool vark, bool gated, int
   const int64_t G = persistent_grid();
   const int64_t rounds_big = (tiles(BM, BN) + G - 1) / G;
   const int64_t rounds_small = (tiles(BM_S, BM_S) + 2 * G - 1) / (2 * G);
-  return 13 * rounds_small < 20 * rounds_big;
+  const int64_t w = K > 0 && K <= 512 ? 11 : 13;
+  return w * rounds_small < 20 * rounds_big;
 }
 
 // dX with a transposed copy of [W1; W3] (moe_set_dx_weight_copy: 0
@@ -1961,7 +1967,7 @@ const char* pass_name(int pass) {
 template <int MODE, int PASS>
 moe_status launch_gemm(hipStream_t s, moe_dtype dt, const FfnPlan& pl, char* ws, GemmParams p) {
   constexpr bool VARK = MODE == M_DW, GATED = MODE == M_FWD1_SWIGLU;
-  const bool small = use_small_tiles(pl, dt, VARK, GATED, p.N, p.M_out);
+  const bool small = use_small_tiles(pl, dt, VARK, GATED, p.N, p.M_out, VARK ? 0 : p.K);
   const int tm = small ? BM_S : BM, tn = small ? BM_S : BN;
   p.ntiles = cdiv(p.N, GATED ? tn / 2 : tn);
   if (VARK) p.mtiles_out = cdiv(p.M_out, tm);
