@@ -199,6 +199,26 @@ def test_split_k_swiglu_later_experts(tiles):
 
 
 @pytest.mark.parametrize("tiles", [1, 2])
+@pytest.mark.parametrize("act", ["relu", "swiglu"])
+def test_weight_gradients_many_empty_experts(tiles, act):
+    """Most experts empty, one with split K and one small (the c3 pattern at
+    a reduced size): gradients exact (ReLU, dyadic) or within tolerance
+    (SwiGLU), and +0.0 for every empty expert."""
+    E, d, f = 12, 512, 1024
+    rows = [0, 0, 3000, 0, 0, 0, 5, 0, 0, 0, 0, 0]
+    dyadic = act == "relu"
+    rows, cap, off, R, P = _problem(E, d, f, rows, [0, 2, 0, 0, 1, 0, 0, 0, 3, 0, 0, 0], act,
+                                    "bf16", dyadic, 90)
+    valid, fw, bw = _oracle(rows, off, P, act, "bf16", E)
+    g = _gpu(rows, cap, off, R, P, act, "bf16", E, d, f, tiles=tiles)
+    _compare(g, valid, fw, bw, act, "bf16", exact=dyadic)
+    empty = [e for e in range(E) if rows[e] == 0]
+    for name in ("dw1", "dw2", "dw3"):
+        if g[name] is not None:
+            assert (g[name][empty] == 0).all() and not np.signbit(g[name][empty]).any(), name
+
+
+@pytest.mark.parametrize("tiles", [1, 2])
 def test_padded_static_rows_match_on_filled_rows(tiles):
     """rows = capacity (padded static-shape baseline): filled rows give the
     same results as rows = fill."""
