@@ -98,8 +98,8 @@ def parse():
                          "bytes as x elsewhere in memory (shows what the previous kernel's "
                          "dirty cache lines cost the next one)")
     ap.add_argument("--tiles", type=int, default=0, choices=[0, 1, 2],
-                    help="bf16 GEMM tiles: 0 the library's choice per product, 1 256x256 "
-                         "only, 2 128x128 only (two workgroups per CU)")
+                    help="GEMM tiles: 0 the library's choice per product, 1 256x256 "
+                         "only (also fp32), 2 128x128 only (bf16; two workgroups per CU)")
     ap.add_argument("--dx-weight-copy", type=int, default=0, choices=[0, 1, 2],
                     help="bf16 dX operand: 0 the library's choice, 1 W1/W3 read K-major, "
                          "2 from a transposed copy made in the backward")

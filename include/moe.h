@@ -494,14 +494,17 @@ moe_status moe_timing_enable(int on);
 int moe_timing_report(char* buf, size_t len);
 
 /*
- * Tile shape of the bf16 expert products (a tuning and testing aid; not part
- * of the method).  mode 0 (default): the library picks per product, from N,
- * the row budget and E, between 256x256 tiles (one workgroup per CU) and
- * 128x128 tiles (two workgroups per CU) -- the latter for products with few
- * tiles per CU; 1: 256x256 only; 2: 128x128 only.  Both kernels add every
- * output's products in the same order, so results are identical bit for bit
- * in every mode.  Process-wide; read when a product is launched.  Returns
- * MOE_EINVAL for other modes. [host]
+ * Tile shape of the expert products (a tuning and testing aid; not part of
+ * the method).  mode 0 (default): the library picks per product.  bf16: from
+ * N, K, the row budget and E, between 256x256 tiles (one workgroup per CU)
+ * and 128x128 tiles (two workgroups per CU) -- the latter for products with
+ * few tiles per CU; both kernels add every output's products in the same
+ * order, so results are identical bit for bit in every mode.  float32: the
+ * forward products of small layers (at most 4096 blocks of 32x32 outputs
+ * for the row budget) run one wavefront per 32x32 block, the others on
+ * 256x256 tiles (the two add in different orders).  1: 256x256 only (both
+ * dtypes); 2: 128x128 only (bf16; float32 as in mode 0).  Process-wide; read
+ * when a product is launched.  Returns MOE_EINVAL for other modes. [host]
  */
 moe_status moe_set_gemm_tiles(int mode);
 

@@ -492,7 +492,8 @@ def moe_timing_enable(on: bool):
 
 
 def moe_set_gemm_tiles(mode: int):
-    """0: automatic tile choice; 1: 256x256 tiles only; 2: 128x128 tiles only."""
+    """0: automatic tile choice; 1: 256x256 tiles only (bf16 and fp32); 2: 128x128 tiles
+    only (bf16)."""
     _check(lib().moe_set_gemm_tiles(int(mode)), "moe_set_gemm_tiles")
 
 

@@ -938,6 +938,112 @@ __global__ __launch_bounds__(kThreads, 1) void ffn_gemm_f32_kernel(const GemmPar
 }
 
 // ---------------------------------------------------------------------------
+// fp32 forward products with few rows
+// ---------------------------------------------------------------------------
+// A 256x256 fp32 tile is one wavefront's 128x64 block on each of eight
+// wavefronts, whatever the rows: with a few dozen rows per expert (fp32
+// matrix cores run at a sixteenth of the bf16 rate) the handful of busy
+// wavefronts sets the time.  Here one wavefront computes one 32x32 output
+// block (gated: 32 hidden units of H1 and of H3) with v_mfma_f32_32x32x2f32,
+// reading both K-contiguous operands straight from memory (64 k at a time,
+// the next 64 in flight), so the work spreads over as many SIMDs as there
+// are blocks.  Lane l supplies row (column) l % 32 and, for the four MFMAs
+// of an 8-wide k step, k values k0 + 4 (l / 32) + j (j = 0..3): every k of
+// the step enters exactly one MFMA, for the A and the B operand alike.  Item = (expert, 32-row block,
+// 32-column block); blocks past the expert's rows or past N exit at once.
+constexpr int kTinyB = 32;
+constexpr int kTinyMaxItems = 4096;
+
+template <int MODE>
+__global__ __launch_bounds__(256) void ffn_gemm_f32_tiny_kernel(const GemmParams p, int E,
+                                                                int mblocks, int nblocks) {
+  constexpr bool GATED = MODE == M_FWD1_SWIGLU;
+  const int lane = threadIdx.x & 63;
+  const int item = static_cast<int>(blockIdx.x) * 4 + (static_cast<int>(threadIdx.x) >> 6);
+  const int per_e = mblocks * nblocks;
+  const int g = item / per_e;
+  if (g >= E) return;
+  const int rem = item - g * per_e;
+  const int m0 = (rem / nblocks) * kTinyB, n0 = (rem % nblocks) * kTinyB;
+  const int rows_g = p.sched->rows[g];
+  if (m0 >= rows_g || n0 >= p.N) return;
+  const int r = lane & 31, kh = 4 * (lane >> 5);
+  const bool arow = m0 + r < rows_g, brow = n0 + r < p.N;
+  const int64_t grow0 = static_cast<int64_t>(p.offsets[g]) + m0;
+  const float* a = reinterpret_cast<const float*>(p.A + (grow0 + (arow ? r : 0)) * p.lda);
+  const int64_t boff = static_cast<int64_t>(g) * p.b_gstride + static_cast<int64_t>(n0 + (brow ? r : 0)) * p.ldb;
+  const float* b1 = reinterpret_cast<const float*>(p.B + boff);
+  const float* b3 = GATED ? reinterpret_cast<const float*>(p.B2 + boff) : b1;
+  const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+  floatx16 c1, c3;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) c1[q] = c3[q] = 0.f;
+  // k in chunks of 64 (8 steps of 8): a chunk's operands are loaded
+  // together, the next chunk's before the current chunk's MFMAs (K is a
+  // multiple of 8; steps past K load zeros)
+  constexpr int kSteps = 8;
+  struct Chunk { float4 a[kSteps], b[kSteps], w[kSteps]; };
+  auto load = [&](int k0, Chunk& c) {
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+      const int kk = k0 + 8 * s + kh;
+      const bool ok = kk < p.K;
+      c.a[s] = arow && ok ? *reinterpret_cast<const float4*>(a + kk) : zero;
+      c.b[s] = brow && ok ? *reinterpret_cast<const float4*>(b1 + kk) : zero;
+      if constexpr (GATED) c.w[s] = brow && ok ? *reinterpret_cast<const float4*>(b3 + kk) : zero;
+    }
+  };
+  auto mma = [&](const Chunk& c) {
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+      c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(c.a[s].x, c.b[s].x, c1, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(c.a[s].y, c.b[s].y, c1, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(c.a[s].z, c.b[s].z, c1, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(c.a[s].w, c.b[s].w, c1, 0, 0, 0);
+      if constexpr (GATED) {
+        c3 = __builtin_amdgcn_mfma_f32_32x32x2f32(c.a[s].x, c.w[s].x, c3, 0, 0, 0);
+        c3 = __builtin_amdgcn_mfma_f32_32x32x2f32(c.a[s].y, c.w[s].y, c3, 0, 0, 0);
+        c3 = __builtin_amdgcn_mfma_f32_32x32x2f32(c.a[s].z, c.w[s].z, c3, 0, 0, 0);
+        c3 = __builtin_amdgcn_mfma_f32_32x32x2f32(c.a[s].w, c.w[s].w, c3, 0, 0, 0);
+      }
+    }
+  };
+  constexpr int KC = 8 * kSteps;
+  Chunk c0, cn;
+  load(0, c0);
+  for (int k0 = 0; k0 < p.K; k0 += 2 * KC) {
+    if (k0 + KC < p.K) load(k0 + KC, cn);
+    mma(c0);
+    if (k0 + KC >= p.K) break;
+    if (k0 + 2 * KC < p.K) load(k0 + 2 * KC, c0);
+    mma(cn);
+  }
+  // accumulator q of lane l: column l % 32, row 8 (q / 4) + 4 (l / 32) + q % 4
+  const int col = n0 + r;
+  if (col >= p.N) return;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int row = m0 + 8 * (q >> 2) + kh + (q & 3);
+    if (row >= rows_g) continue;
+    const int64_t grow = static_cast<int64_t>(p.offsets[g]) + row;
+    float* cp = reinterpret_cast<float*>(p.C + grow * p.ldc) + col;
+    if constexpr (MODE == M_FWD1_SWIGLU) {
+      const float h1 = c1[q], h3 = c3[q];
+      if (p.H1) {
+        reinterpret_cast<float*>(p.H1 + grow * p.ldh)[col] = h1;
+        reinterpret_cast<float*>(p.H3 + grow * p.ldh)[col] = h3;
+      }
+      *cp = h1 * sigm(h1) * h3;
+    } else if constexpr (MODE == M_FWD1) {
+      if (p.H1) reinterpret_cast<float*>(p.H1 + grow * p.ldh)[col] = c1[q];
+      *cp = act_f(c1[q], p.act);
+    } else {
+      *cp = c1[q];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // bf16 products: four wavefronts of 128x128
 // ---------------------------------------------------------------------------
 // bf16 layers run every product on 4 wavefronts, one per SIMD, each holding a
@@ -1979,6 +2085,19 @@ moe_status launch_gemm(hipStream_t s, moe_dtype dt, const FfnPlan& pl, char* ws,
                                        p.ntiles;
   const int64_t full = (small ? 2 : 1) * static_cast<int64_t>(persistent_grid());
   const int grid = static_cast<int>(std::min(full, std::max<int64_t>(kXcds, (max_items + kXcds - 1) / kXcds * kXcds)));
+  if constexpr ((MODE == M_FWD1 || MODE == M_FWD1_SWIGLU || MODE == M_STORE) &&
+                (PASS == P_FWD_H || PASS == P_FWD_Y)) {
+    // fp32 forward with few rows: one wavefront per 32x32 output block
+    const int64_t mb = cdiv(pl.rows_alloc, kTinyB), nb = cdiv(p.N, kTinyB);
+    const int64_t items = static_cast<int64_t>(pl.E) * mb * nb;
+    if (dt == MOE_F32 && g_tile_mode != 1 && items <= kTinyMaxItems) {
+      MOE_TIMED(pass_name(PASS), s);
+      ffn_gemm_f32_tiny_kernel<MODE><<<static_cast<unsigned>(cdiv(items, 4)), 256, 0, s>>>(
+          p, pl.E, static_cast<int>(mb), static_cast<int>(nb));
+      MOE_LAUNCH_CHECK();
+      return MOE_OK;
+    }
+  }
   MOE_TIMED(pass_name(PASS), s);
   if (dt == MOE_BF16 && small)
     ffn_gemm16_kernel<MODE, PASS, TileSmall><<<grid, kThreads16, 0, s>>>(p);

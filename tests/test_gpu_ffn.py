@@ -4,7 +4,8 @@ backward against the CPU oracle, through the C ABI.
 The bf16 cases run on both GEMM kernels (moe_set_gemm_tiles: 1 = 256x256
 tiles, 2 = 128x128 tiles, two workgroups per CU) and with dX reading the
 weights K-major or from their transposed copy (moe_set_dx_weight_copy); f32
-layers have one kernel.
+cases run with the small-layer forward kernel (mode 0) and without it
+(mode 1).
 
 ReLU cases use dyadic inputs (x, dy in {-2..2}/4, weights in {-2..2}/16):
 every GEMM partial sum is exactly representable in fp32, so the kernels and
@@ -126,9 +127,11 @@ CASES = [
 
 
 # (dtype, tile mode, dX weight copy): bf16 on both kernels, each with dX
-# reading the weights K-major (1) and from the transposed copy (2); f32 on
-# its one kernel
-DT_TILES = [("f32", 0, 0), ("bf16", 1, 1), ("bf16", 2, 1), ("bf16", 1, 2), ("bf16", 2, 2)]
+# reading the weights K-major (1) and from the transposed copy (2); f32 with
+# its small-layer forward kernel (mode 0: one wavefront per 32x32 block) and
+# on 256x256 tiles only (mode 1)
+DT_TILES = [("f32", 0, 0), ("f32", 1, 0), ("bf16", 1, 1), ("bf16", 2, 1), ("bf16", 1, 2),
+            ("bf16", 2, 2)]
 
 
 @pytest.mark.parametrize("dt,tiles,wcopy", DT_TILES)
