@@ -401,23 +401,33 @@ __global__ __launch_bounds__(64) void gate_fwd_f32_kernel(
   const int t = blockIdx.x * 64 + lane;
   if (t < T) {
     // the token's row is read 16 bytes at a time (d is a multiple of 8, rows
-    // start 32-byte aligned) and scored against 8 experts per pass: 8
-    // independent sums, each over i in order; w_g is the same for every lane
+    // start 32-byte aligned), eight such loads issued before they are used,
+    // and scored against 8 experts per pass: 8 independent sums, each over i
+    // in order; w_g is the same for every lane
     const float* xr = x + static_cast<size_t>(t) * d;
+    constexpr int kXb = 8;   // row vectors in flight
     for (int e0 = 0; e0 < E; e0 += 8) {
       float a[8];
 #pragma unroll
       for (int q = 0; q < 8; ++q) a[q] = 0.f;
-      for (int i = 0; i < d; i += 4) {
-        const float4 xv = *reinterpret_cast<const float4*>(xr + i);
+      for (int i0 = 0; i0 < d; i0 += 4 * kXb) {
+        float4 xv[kXb];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          if (e0 + q < E) {
-            const float4 w = *reinterpret_cast<const float4*>(wg + static_cast<size_t>(e0 + q) * d + i);
-            a[q] = fmaf(xv.x, w.x, a[q]);
-            a[q] = fmaf(xv.y, w.y, a[q]);
-            a[q] = fmaf(xv.z, w.z, a[q]);
-            a[q] = fmaf(xv.w, w.w, a[q]);
+        for (int u = 0; u < kXb; ++u)
+          if (i0 + 4 * u < d) xv[u] = *reinterpret_cast<const float4*>(xr + i0 + 4 * u);
+#pragma unroll
+        for (int u = 0; u < kXb; ++u) {
+          const int i = i0 + 4 * u;
+          if (i >= d) break;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            if (e0 + q < E) {
+              const float4 w = *reinterpret_cast<const float4*>(wg + static_cast<size_t>(e0 + q) * d + i);
+              a[q] = fmaf(xv[u].x, w.x, a[q]);
+              a[q] = fmaf(xv[u].y, w.y, a[q]);
+              a[q] = fmaf(xv[u].z, w.z, a[q]);
+              a[q] = fmaf(xv[u].w, w.w, a[q]);
+            }
           }
         }
       }
