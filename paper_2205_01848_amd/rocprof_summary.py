@@ -51,6 +51,11 @@ def short_name(name: str) -> str:
         small = re.search(r"Tile16<4, 4, 2>", name) is not None
         return (PASS_NAMES[int(m.group(3))] + ("_f32" if m.group(1) == "_f32" else "")
                 + ("_t128" if small else ""))
+    # fp32 forward of small layers: ffn_gemm_f32_tiny_kernel<MODE> (modes 0, 1:
+    # the first product, 2: the second)
+    m = re.search(r"ffn_gemm_f32_tiny_kernel<(\d+)>", name)
+    if m:
+        return ("gemm_fwd_y" if m.group(1) == "2" else "gemm_fwd_h") + "_f32_tiny"
     m = re.search(r"moe::(?:\(anonymous namespace\)::)?(\w+)(<[^(]*>)?", name)
     if m:
         targs = (m.group(2) or "").replace("unsigned short", "bf16").replace("float", "f32")
