@@ -2271,7 +2271,8 @@ extern "C" moe_status moe_expert_ffn_bwd(void* stream, moe_dtype dt, moe_act act
   char* wt13 = ws + pl.o_wt13;
   if (wt) MOE_TRY(launch_transpose_w(s, E, w1, sw ? w3 : nullptr, f, sw ? f : 0, d, wt13));
 
-  // dx_disp = [dH1 | dH3] [W1; W3] (W1, W3 read K-major, W3 from k = f on)
+  // dx_disp = [dH1 | dH3] [W1; W3]: from the transposed copy, or W1, W3 read
+  // K-major (W3 from k = f on)
   auto launch_dx = [&]() -> moe_status {
     if (wt) {
       GemmParams q = base_params(pl, offsets, ws);
