@@ -310,8 +310,10 @@ def test_combine_and_backward(dt, k, d):
     assert (to_np(y)[(dest < 0).all(axis=1)] == 0).all()
 
 
+# gates of 4 to 64 experts; 40 leaves a partial group of eight experts
 @pytest.mark.parametrize("dt,E,k,renorm", [("bf16", 8, 2, 1), ("bf16", 64, 1, 0), ("f32", 4, 1, 0),
-                                           ("bf16", 16, 3, 1)])
+                                           ("bf16", 16, 3, 1), ("f32", 40, 2, 0),
+                                           ("bf16", 40, 3, 1)])
 def test_gate_backward(dt, E, k, renorm):
     rng = np.random.default_rng(60 + E)
     T, d = 1100, 264
