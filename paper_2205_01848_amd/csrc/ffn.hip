@@ -14,7 +14,8 @@
 //    products in the same order.
 //  * fp32 layers: 8 wavefronts of 128x64 on v_mfma_f32_32x32x2f32 in two
 //    ping-pong teams, one team's MFMAs overlapping the other's LDS reads
-//    (ffn_gemm_f32_kernel).
+//    (ffn_gemm_f32_kernel); the forward of small fp32 layers instead runs
+//    one wavefront per 32x32 output block (ffn_gemm_f32_tiny_kernel).
 //  * var-M products (forward H, Y; backward dA, dX): the M dimension of
 //    expert e is its row count, read on the device; tiles are listed by a
 //    one-workgroup schedule kernel, so no host synchronisation is needed.
